@@ -1,0 +1,68 @@
+"""Named workloads: one tensor-parallel rank's share of a row-parallel
+GEMM-ReduceScatter, with the shapes of the paper's LLM projections.
+
+Each rank holds A (M x K_local) and B (K_local x N) and emits an M x N partial;
+the output is split into P equal row chunks.  The synthetic peer partials
+stand in for the other P-1 ranks and are drawn with the variance a real
+partial of the same shape would have: with A, B ~ N(0, s^2) a K-term dot
+product has standard deviation s*s*sqrt(K).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+from .inputs import BASE_SEED, Dist, Problem, make_problem
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    M: int
+    N: int
+    K: int
+    P: int
+    ab: Dist
+    peer: Dist
+    note: str = ""
+
+    @property
+    def flops(self) -> float:
+        return 2.0 * self.M * self.N * self.K
+
+    def problem(self, seed: int = BASE_SEED) -> Problem:
+        return make_problem(self.M, self.N, self.K, self.P, self.ab, self.peer, seed)
+
+
+def _llm(name, M, K, N, P, note):
+    s = 0.02
+    return Workload(name, M, N, K, P, Dist("normal", s), Dist("normal", s * s * math.sqrt(K)), note)
+
+
+WORKLOADS = {
+    w.name: w
+    for w in [
+        # U[-1,1] entries: a 256-term dot product has std sqrt(256/9).
+        Workload("tiny_512x256x1024_p2", 512, 1024, 256, 2,
+                 Dist("uniform", 1.0), Dist("normal", math.sqrt(256 / 9)),
+                 "small parity case, two row chunks of 256 x 1024"),
+        _llm("llama7b_mlp_down_tp8", 4096, 1376, 4096, 8,
+             "Llama-7B MLP down projection (K = 11008 / 8), 4096 tokens"),
+        _llm("llama70b_attn_out_tp8", 8192, 1024, 8192, 8,
+             "Llama-3-70B attention output projection, 8192 tokens"),
+        _llm("llama70b_mlp_down_tp8", 16384, 3584, 8192, 8,
+             "Llama-3-70B MLP down projection, 16384 tokens"),
+    ]
+}
+
+# Schedule / CU-split sweep: M = N = 8192, K_local in {512, 2048}, P in {2, 4, 8}.
+for _K in (512, 2048):
+    for _P in (2, 4, 8):
+        _w = _llm(f"sweep_8192x{_K}x8192_p{_P}", 8192, _K, 8192, _P,
+                  "budget / tile-order sweep window (the paper's two K windows)")
+        WORKLOADS[_w.name] = _w
+
+BENCH_WORKLOAD = "llama7b_mlp_down_tp8"
+SMALL_WORKLOAD = "tiny_512x256x1024_p2"
+
+__all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "SMALL_WORKLOAD", "BASE_SEED"]
