@@ -124,3 +124,25 @@ def error_bound_rows(A_bits, B_bits, peer_bits, rows) -> np.ndarray:
 def paper_gate(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
     """Elementwise pass mask of the paper's correctness gate."""
     return np.abs(got - ref) <= PAPER_ATOL + PAPER_RTOL * np.abs(ref)
+
+
+def f32_to_bf16_rne_bits(x) -> np.ndarray:
+    """Round float32 values to bfloat16, nearest-even, returning the bits:
+    keep the upper 16 bits after adding 0x7FFF plus the lowest kept bit
+    (ties go to the even neighbour); NaN stays a quiet NaN."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    rounded = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    nan = np.isnan(f)
+    return np.where(nan, ((u >> 16) | 0x40).astype(np.uint16), rounded)
+
+
+def reduce_tile_f32(partial_bits, peer_bits) -> np.ndarray:
+    """The reducer's own arithmetic on bf16 contributions (Section 4.2,
+    ReduceTile): start from the local contribution, add the peers one at a
+    time in rank order, each addition rounded to float32, then round the sum
+    to bfloat16.  Returns bf16 bits; bit-exact by definition."""
+    acc = bf16_to_f64(partial_bits).astype(np.float32)
+    for pb in peer_bits:
+        acc = (acc + bf16_to_f64(pb).astype(np.float32)).astype(np.float32)
+    return f32_to_bf16_rne_bits(acc)

@@ -1,0 +1,578 @@
+// entwine.hip - host launcher and C ABI of libentwine.so (declared in
+// include/entwine.h).
+//
+// One call of the fused path (paper Section 4.1): fork the reduce stream off
+// the GEMM stream, enqueue the producer GEMM on the GEMM stream and, on the
+// reduce stream, the synthetic peer-flag publication followed by the tile
+// reducer, then join the reduce stream back into the GEMM stream.  The GEMM
+// is enqueued first, so it can never be starved by waiting reducer
+// workgroups: if both streams land on one hardware queue the reducer simply
+// runs after the GEMM.  Flags are never cleared between calls; every call
+// takes a fresh epoch and a flag is ready when it holds that epoch (the
+// paper resets flags before each invocation).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/entwine.h"
+#include "gemm_producer.h"
+#include "tile_order.h"
+#include "tile_reducer.h"
+
+using namespace entwine;
+
+namespace {
+
+constexpr int kRing = 256;
+
+struct TimingSlot {
+  hipEvent_t start = nullptr, gemm_end = nullptr, red_end = nullptr;
+  bool has_gemm = false, has_red = false;
+};
+
+struct CfgShape {
+  int BM, BN;
+};
+constexpr CfgShape kCfgShapes[ENTWINE_GEMM_NUM_CFGS] = {{256, 256}, {256, 128}, {128, 256}, {128, 128}};
+
+}  // namespace
+
+struct entwine_ctx {
+  int device = 0;
+  int64_t M = 0, N = 0, K = 0;
+  int P = 1;
+  int cus = 0;
+  int64_t ntiles = 0;
+  int* flags = nullptr;        // local tile flags
+  int* peer_flags = nullptr;   // (P-1) x ntiles
+  int* status = nullptr;       // {code, tile, src, pad}
+  uint16_t* scratch = nullptr; // M x N partial when the caller passes none
+  uint32_t epoch = 0;
+  uint64_t ticks_per_us = 100;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  TimingSlot ring[kRing];
+  int64_t ncalls = 0;          // calls with record_timing
+  hipStream_t last_stream = nullptr;
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+entwine_status fail(entwine_ctx* ctx, entwine_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf;
+  g_err = buf;
+  return s;
+}
+
+#define HIP_OR_FAIL(ctx, call)                                                           \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess) return fail(ctx, ENTWINE_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+entwine_status validate_shape(entwine_ctx* ctx, int64_t M, int64_t N, int64_t K, int32_t P) {
+  if (P < 1 || P > ENTWINE_MAX_P) return fail(ctx, ENTWINE_EINVAL, "P=%d outside [1, %d]", P, ENTWINE_MAX_P);
+  if (M <= 0 || N <= 0 || K <= 0) return fail(ctx, ENTWINE_EINVAL, "M, N, K must be positive");
+  if (M % (int64_t(ENTWINE_TILE) * P)) return fail(ctx, ENTWINE_EINVAL, "M=%lld is not a multiple of 128*P", (long long)M);
+  if (N % ENTWINE_TILE) return fail(ctx, ENTWINE_EINVAL, "N=%lld is not a multiple of 128", (long long)N);
+  if (K % 8) return fail(ctx, ENTWINE_EINVAL, "K=%lld is not a multiple of 8", (long long)K);
+  if (M > (1 << 30) || N > (1 << 30) || K > (1 << 30)) return fail(ctx, ENTWINE_EINVAL, "dimension too large");
+  return ENTWINE_OK;
+}
+
+int default_gemm_cfg(int64_t M, int64_t N, int P) {
+  for (int c = 0; c < ENTWINE_GEMM_NUM_CFGS; ++c)
+    if ((M / P) % kCfgShapes[c].BM == 0 && N % kCfgShapes[c].BN == 0) return c;
+  return ENTWINE_GEMM_128x128;
+}
+
+struct Resolved {
+  int order, gemm_cfg, BM, BN, x, threads, withhold, timing;
+  uint64_t timeout_us;
+};
+
+entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_t dest,
+                       const entwine_config* cfg, int cus, Resolved* r) {
+  entwine_config c;
+  entwine_config_default(&c);
+  if (cfg) c = *cfg;
+  if (dest != ENTWINE_DEST_ALL && (dest < 0 || dest >= P))
+    return fail(ctx, ENTWINE_EINVAL, "dest=%d outside [-1, P)", dest);
+  if (c.order < 0 || c.order > 2) return fail(ctx, ENTWINE_EINVAL, "unknown order %d", c.order);
+  if (c.gemm_cfg < -1 || c.gemm_cfg >= ENTWINE_GEMM_NUM_CFGS) return fail(ctx, ENTWINE_EINVAL, "unknown gemm_cfg %d", c.gemm_cfg);
+  if (c.reduce_threads != 0 && c.reduce_threads != 128 && c.reduce_threads != 256 && c.reduce_threads != 512)
+    return fail(ctx, ENTWINE_EINVAL, "reduce_threads must be 128, 256 or 512");
+  if (c.reduce_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "reduce_wgs must be >= 0");
+  if (c.timeout_us < 0) return fail(ctx, ENTWINE_EINVAL, "timeout_us must be >= 0");
+  if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
+  r->order = c.order;
+  r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
+  r->BM = kCfgShapes[r->gemm_cfg].BM;
+  r->BN = kCfgShapes[r->gemm_cfg].BN;
+  if ((M / P) % r->BM || N % r->BN)
+    return fail(ctx, ENTWINE_EUNSUPPORTED, "block %dx%d does not divide the %lldx%lld chunk", r->BM, r->BN,
+                (long long)(M / P), (long long)N);
+  const int Q = tiles_per_partition(int(M), int(N), P);
+  int x = c.reduce_wgs > 0 ? c.reduce_wgs : 16;
+  const int cap_cus = std::max(1, (cus > 1 ? cus - 1 : 255));
+  if (dest == ENTWINE_DEST_ALL) {
+    x = std::min(x, Q * P);
+    x = ((x + P - 1) / P) * P;
+    while (x > P && x > cap_cus) x -= P;
+  } else {
+    x = std::min(std::min(x, Q), cap_cus);
+  }
+  r->x = std::max(x, 1);
+  r->threads = c.reduce_threads ? c.reduce_threads : 256;
+  r->withhold = c.withhold_peer;
+  r->timing = c.record_timing;
+  r->timeout_us = c.timeout_us ? uint64_t(c.timeout_us) : 2000000ull;
+  return ENTWINE_OK;
+}
+
+entwine_status check_matrix(entwine_ctx* ctx, const void* p, int64_t ld, int64_t cols, const char* name) {
+  if (!p) return fail(ctx, ENTWINE_EINVAL, "%s is NULL", name);
+  if (!aligned16(p)) return fail(ctx, ENTWINE_EINVAL, "%s is not 16-byte aligned", name);
+  if (ld < cols) return fail(ctx, ENTWINE_EINVAL, "ld of %s (%lld) < %lld", name, (long long)ld, (long long)cols);
+  if (ld % 8) return fail(ctx, ENTWINE_EINVAL, "ld of %s is not a multiple of 8", name);
+  return ENTWINE_OK;
+}
+
+#define CHECK(x)                       \
+  do {                                 \
+    entwine_status s_ = (x);           \
+    if (s_ != ENTWINE_OK) return s_;   \
+  } while (0)
+
+typedef void (*GemmKernel)(GemmArgs);
+GemmKernel gemm_kernel(int cfg) {
+  switch (cfg) {
+    case 0: return gemm_producer<256, 256>;
+    case 1: return gemm_producer<256, 128>;
+    case 2: return gemm_producer<128, 256>;
+    default: return gemm_producer<128, 128>;
+  }
+}
+int gemm_lds_bytes(int cfg) {
+  switch (cfg) {
+    case 0: return GemmShape<256, 256>::LDS_BYTES;
+    case 1: return GemmShape<256, 128>::LDS_BYTES;
+    case 2: return GemmShape<128, 256>::LDS_BYTES;
+    default: return GemmShape<128, 128>::LDS_BYTES;
+  }
+}
+
+typedef void (*ReduceKernel)(ReduceArgs);
+template <int T>
+ReduceKernel reduce_kernel_p(int P) {
+  switch (P) {
+    case 1: return tile_reducer<T, 1>;
+    case 2: return tile_reducer<T, 2>;
+    case 3: return tile_reducer<T, 3>;
+    case 4: return tile_reducer<T, 4>;
+    case 5: return tile_reducer<T, 5>;
+    case 6: return tile_reducer<T, 6>;
+    case 7: return tile_reducer<T, 7>;
+    default: return tile_reducer<T, 8>;
+  }
+}
+ReduceKernel reduce_kernel(int threads, int P) {
+  if (threads == 128) return reduce_kernel_p<128>(P);
+  if (threads == 512) return reduce_kernel_p<512>(P);
+  return reduce_kernel_p<256>(P);
+}
+
+uint32_t next_epoch(entwine_ctx* ctx) {
+  ctx->epoch += 1;
+  if (ctx->epoch == 0 || ctx->epoch > 0x7fffffffu) ctx->epoch = 1;  // flags compare as int
+  return ctx->epoch;
+}
+
+entwine_status ensure_scratch(entwine_ctx* ctx) {
+  if (ctx->scratch) return ENTWINE_OK;
+  hipError_t e = hipMalloc(&ctx->scratch, size_t(ctx->M) * size_t(ctx->N) * 2);
+  if (e != hipSuccess) {
+    ctx->scratch = nullptr;
+    return fail(ctx, ENTWINE_ENOMEM, "partial scratch: %s", hipGetErrorString(e));
+  }
+  return ENTWINE_OK;
+}
+
+TimingSlot* timing_slot(entwine_ctx* ctx, const Resolved& r) {
+  if (!r.timing) return nullptr;
+  TimingSlot* s = &ctx->ring[ctx->ncalls % kRing];
+  ctx->ncalls++;
+  s->has_gemm = s->has_red = false;
+  return s;
+}
+
+entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t lda, const void* B,
+                           int64_t ldb, void* C, int64_t ldc, bool publish, uint32_t epoch,
+                           hipStream_t s) {
+  GemmArgs g;
+  g.A = static_cast<const uint16_t*>(A);
+  g.B = static_cast<const uint16_t*>(B);
+  g.C = static_cast<uint16_t*>(C);
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.M = int(ctx->M);
+  g.N = int(ctx->N);
+  g.K = int(ctx->K);
+  g.P = ctx->P;
+  g.order = r.order;
+  g.flags = publish ? ctx->flags : nullptr;
+  g.epoch = epoch;
+  const int nblocks = int((ctx->M / r.BM) * (ctx->N / r.BN));
+  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(nblocks), dim3(256), gemm_lds_bytes(r.gemm_cfg), s, g);
+  HIP_OR_FAIL(ctx, hipGetLastError());
+  return ENTWINE_OK;
+}
+
+entwine_status launch_publish(entwine_ctx* ctx, int* flags, int64_t n, int64_t per, int skip, uint32_t epoch,
+                              hipStream_t s) {
+  if (n <= 0) return ENTWINE_OK;
+  const int blocks = int(std::min<int64_t>((n + 255) / 256, 1024));
+  hipLaunchKernelGGL(publish_fill, dim3(blocks), dim3(256), 0, s, flags, n, per, skip, epoch);
+  HIP_OR_FAIL(ctx, hipGetLastError());
+  return ENTWINE_OK;
+}
+
+entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* partial, int64_t ldc,
+                             const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
+                             uint32_t epoch, hipStream_t s) {
+  ReduceArgs ra;
+  memset(&ra, 0, sizeof ra);
+  ra.partial = static_cast<const uint16_t*>(partial);
+  for (int q = 0; q < ctx->P - 1; ++q) ra.peers[q] = static_cast<const uint16_t*>(peers[q]);
+  ra.out = static_cast<uint16_t*>(out);
+  ra.ldc = ldc;
+  ra.ldp = ldp;
+  ra.ldo = ldo;
+  ra.M = int(ctx->M);
+  ra.N = int(ctx->N);
+  ra.dest = dest;
+  ra.x = r.x;
+  ra.BM = r.BM;
+  ra.BN = r.BN;
+  ra.flags = ctx->flags;
+  ra.peer_flags = ctx->peer_flags;
+  ra.epoch = epoch;
+  ra.status = ctx->status;
+  ra.timeout_ticks = r.timeout_us * ctx->ticks_per_us;
+  hipLaunchKernelGGL(reduce_kernel(r.threads, ctx->P), dim3(r.x), dim3(r.threads), 0, s, ra);
+  HIP_OR_FAIL(ctx, hipGetLastError());
+  return ENTWINE_OK;
+}
+
+entwine_status check_peers(entwine_ctx* ctx, const void* const* peers, int64_t ldp) {
+  if (ctx->P == 1) return ENTWINE_OK;
+  if (!peers) return fail(ctx, ENTWINE_EINVAL, "peers is NULL with P > 1");
+  for (int q = 0; q < ctx->P - 1; ++q) CHECK(check_matrix(ctx, peers[q], ldp, ctx->N, "peer"));
+  return ENTWINE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void entwine_config_default(entwine_config* cfg) {
+  if (!cfg) return;
+  cfg->order = ENTWINE_ORDER_INTERLEAVED;
+  cfg->gemm_cfg = -1;
+  cfg->reduce_wgs = 0;
+  cfg->reduce_threads = 0;
+  cfg->timeout_us = 0;
+  cfg->withhold_peer = -1;
+  cfg->record_timing = 0;
+  cfg->reserved = 0;
+}
+
+int32_t entwine_abi_version(void) { return ENTWINE_ABI_VERSION; }
+
+const char* entwine_status_string(entwine_status s) {
+  switch (s) {
+    case ENTWINE_OK: return "ENTWINE_OK";
+    case ENTWINE_EINVAL: return "ENTWINE_EINVAL";
+    case ENTWINE_EUNSUPPORTED: return "ENTWINE_EUNSUPPORTED";
+    case ENTWINE_ENOMEM: return "ENTWINE_ENOMEM";
+    case ENTWINE_EHIP: return "ENTWINE_EHIP";
+    case ENTWINE_ETIMEOUT: return "ENTWINE_ETIMEOUT";
+  }
+  return "ENTWINE_UNKNOWN";
+}
+
+const char* entwine_last_error(const entwine_ctx* ctx) { return ctx ? ctx->err.c_str() : g_err.c_str(); }
+
+entwine_status entwine_validate(int64_t M, int64_t N, int64_t K, int32_t P, int32_t dest,
+                                const entwine_config* cfg) {
+  CHECK(validate_shape(nullptr, M, N, K, P));
+  Resolved r;
+  return resolve(nullptr, M, N, P, dest, cfg, 256, &r);
+}
+
+entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, int64_t N, int64_t K,
+                                  int32_t P) {
+  if (!out) return fail(nullptr, ENTWINE_EINVAL, "out is NULL");
+  *out = nullptr;
+  CHECK(validate_shape(nullptr, M, N, K, P));
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev)
+    return fail(nullptr, ENTWINE_EINVAL, "device %d not available", device);
+  entwine_ctx* c = new entwine_ctx();
+  c->device = device;
+  c->M = M;
+  c->N = N;
+  c->K = K;
+  c->P = P;
+  c->ntiles = (M / ENTWINE_TILE) * (N / ENTWINE_TILE);
+  auto bail = [&](entwine_status s) {
+    entwine_ctx_destroy(c);
+    return s;
+  };
+  if (hipSetDevice(device) != hipSuccess) return bail(fail(nullptr, ENTWINE_EHIP, "hipSetDevice failed"));
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return bail(fail(nullptr, ENTWINE_EHIP, "device properties"));
+  c->cus = prop.multiProcessorCount;
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, device) == hipSuccess && khz > 0)
+    c->ticks_per_us = uint64_t(khz) / 1000 ? uint64_t(khz) / 1000 : 1;
+  const size_t fbytes = size_t(c->ntiles) * sizeof(int);
+  if (hipMalloc(&c->flags, fbytes) != hipSuccess ||
+      hipMalloc(&c->peer_flags, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
+      hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess)
+    return bail(fail(nullptr, ENTWINE_ENOMEM, "flag allocation failed"));
+  if (hipMemset(c->flags, 0, fbytes) != hipSuccess ||
+      hipMemset(c->peer_flags, 0, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
+      hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess)
+    return bail(fail(nullptr, ENTWINE_EHIP, "flag initialisation failed"));
+  if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+    return bail(fail(nullptr, ENTWINE_EHIP, "event creation failed"));
+  for (auto& s : c->ring)
+    if (hipEventCreate(&s.start) != hipSuccess || hipEventCreate(&s.gemm_end) != hipSuccess ||
+        hipEventCreate(&s.red_end) != hipSuccess)
+      return bail(fail(nullptr, ENTWINE_EHIP, "event creation failed"));
+  for (int cfg = 0; cfg < ENTWINE_GEMM_NUM_CFGS; ++cfg)
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel(cfg)),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes(cfg)) != hipSuccess)
+      return bail(fail(nullptr, ENTWINE_EHIP, "LDS size attribute failed"));
+  if (hipDeviceSynchronize() != hipSuccess) return bail(fail(nullptr, ENTWINE_EHIP, "initial sync failed"));
+  *out = c;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
+  if (!ctx) return ENTWINE_OK;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  if (ctx->flags) (void)hipFree(ctx->flags);
+  if (ctx->peer_flags) (void)hipFree(ctx->peer_flags);
+  if (ctx->status) (void)hipFree(ctx->status);
+  if (ctx->scratch) (void)hipFree(ctx->scratch);
+  if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
+  if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
+  for (auto& s : ctx->ring) {
+    if (s.start) (void)hipEventDestroy(s.start);
+    if (s.gemm_end) (void)hipEventDestroy(s.gemm_end);
+    if (s.red_end) (void)hipEventDestroy(s.red_end);
+  }
+  delete ctx;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, const void* B, int64_t ldb,
+                               const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
+                               void* partial, int64_t ldc, const entwine_config* cfg, void* gemm_stream,
+                               void* reduce_stream) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  Resolved r;
+  CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, dest, cfg, ctx->cus, &r));
+  CHECK(check_matrix(ctx, A, lda, ctx->K, "A"));
+  CHECK(check_matrix(ctx, B, ldb, ctx->N, "B"));
+  CHECK(check_matrix(ctx, out, ldo, ctx->N, "out"));
+  CHECK(check_peers(ctx, peers, ldp));
+  if (partial) {
+    CHECK(check_matrix(ctx, partial, ldc, ctx->N, "partial"));
+  } else {
+    CHECK(ensure_scratch(ctx));
+    partial = ctx->scratch;
+    ldc = ctx->N;
+  }
+  HIP_OR_FAIL(ctx, hipSetDevice(ctx->device));
+  hipStream_t gs = static_cast<hipStream_t>(gemm_stream);
+  hipStream_t rs = static_cast<hipStream_t>(reduce_stream);
+  const bool fused = gs != rs;
+  const uint32_t epoch = next_epoch(ctx);
+  TimingSlot* ts = timing_slot(ctx, r);
+
+  if (fused) HIP_OR_FAIL(ctx, hipEventRecord(ctx->ev_fork, gs));
+  if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, gs));
+  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, gs));
+  if (ts) {
+    HIP_OR_FAIL(ctx, hipEventRecord(ts->gemm_end, gs));
+    ts->has_gemm = true;
+  }
+  if (fused) HIP_OR_FAIL(ctx, hipStreamWaitEvent(rs, ctx->ev_fork, 0));
+  CHECK(launch_publish(ctx, ctx->peer_flags, ctx->ntiles * (ctx->P - 1), ctx->ntiles, r.withhold, epoch, rs));
+  CHECK(launch_reduce(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch, rs));
+  if (ts) {
+    HIP_OR_FAIL(ctx, hipEventRecord(ts->red_end, rs));
+    ts->has_red = true;
+  }
+  if (fused) {
+    HIP_OR_FAIL(ctx, hipEventRecord(ctx->ev_join, rs));
+    HIP_OR_FAIL(ctx, hipStreamWaitEvent(gs, ctx->ev_join, 0));
+  }
+  ctx->last_stream = gs;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_gemm_only(entwine_ctx* ctx, const void* A, int64_t lda, const void* B, int64_t ldb,
+                                 void* partial, int64_t ldc, const entwine_config* cfg, void* stream) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  Resolved r;
+  CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, 0, cfg, ctx->cus, &r));
+  CHECK(check_matrix(ctx, A, lda, ctx->K, "A"));
+  CHECK(check_matrix(ctx, B, ldb, ctx->N, "B"));
+  if (partial) {
+    CHECK(check_matrix(ctx, partial, ldc, ctx->N, "partial"));
+  } else {
+    CHECK(ensure_scratch(ctx));
+    partial = ctx->scratch;
+    ldc = ctx->N;
+  }
+  HIP_OR_FAIL(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint32_t epoch = next_epoch(ctx);
+  TimingSlot* ts = timing_slot(ctx, r);
+  if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, s));
+  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, s));
+  if (ts) {
+    HIP_OR_FAIL(ctx, hipEventRecord(ts->gemm_end, s));
+    ts->has_gemm = true;
+  }
+  ctx->last_stream = s;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_reduce_only(entwine_ctx* ctx, const void* partial, int64_t ldc, const void* const* peers,
+                                   int64_t ldp, int32_t dest, void* out, int64_t ldo, const entwine_config* cfg,
+                                   void* stream) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  Resolved r;
+  CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, dest, cfg, ctx->cus, &r));
+  CHECK(check_matrix(ctx, partial, ldc, ctx->N, "partial"));
+  CHECK(check_matrix(ctx, out, ldo, ctx->N, "out"));
+  CHECK(check_peers(ctx, peers, ldp));
+  HIP_OR_FAIL(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint32_t epoch = next_epoch(ctx);
+  TimingSlot* ts = timing_slot(ctx, r);
+  CHECK(launch_publish(ctx, ctx->flags, ctx->ntiles, ctx->ntiles, -1, epoch, s));
+  CHECK(launch_publish(ctx, ctx->peer_flags, ctx->ntiles * (ctx->P - 1), ctx->ntiles, r.withhold, epoch, s));
+  if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, s));
+  CHECK(launch_reduce(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch, s));
+  if (ts) {
+    HIP_OR_FAIL(ctx, hipEventRecord(ts->red_end, s));
+    ts->has_red = true;
+  }
+  ctx->last_stream = s;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_query_status(entwine_ctx* ctx, int32_t* code, int32_t* tile, int32_t* src) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  HIP_OR_FAIL(ctx, hipSetDevice(ctx->device));
+  HIP_OR_FAIL(ctx, hipDeviceSynchronize());
+  int h[4] = {0, 0, 0, 0};
+  HIP_OR_FAIL(ctx, hipMemcpy(h, ctx->status, sizeof h, hipMemcpyDeviceToHost));
+  HIP_OR_FAIL(ctx, hipMemset(ctx->status, 0, sizeof h));
+  if (code) *code = h[0];
+  if (tile) *tile = h[0] ? h[1] : -1;
+  if (src) *src = h[0] ? h[2] : -2;
+  if (h[0]) return fail(ctx, ENTWINE_ETIMEOUT, "reducer wait expired on tile %d (source %d)", h[1], h[2]);
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_ms, float* reduce_ms,
+                                   float* e2e_ms) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  if (back < 0 || back >= kRing || back >= ctx->ncalls) return fail(ctx, ENTWINE_EINVAL, "no such timed call");
+  TimingSlot& s = ctx->ring[(ctx->ncalls - 1 - back) % kRing];
+  float g = -1.f, rd = -1.f, e = -1.f;
+  if (s.has_gemm) {
+    HIP_OR_FAIL(ctx, hipEventSynchronize(s.gemm_end));
+    HIP_OR_FAIL(ctx, hipEventElapsedTime(&g, s.start, s.gemm_end));
+  }
+  if (s.has_red) {
+    HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
+    HIP_OR_FAIL(ctx, hipEventElapsedTime(&rd, s.start, s.red_end));
+  }
+  e = std::max(g, rd);
+  if (gemm_ms) *gemm_ms = g;
+  if (reduce_ms) *reduce_ms = rd;
+  if (e2e_ms) *e2e_ms = e;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_tile_schedule(int32_t order, int64_t M, int64_t N, int32_t P, int32_t BM, int32_t BN,
+                                     int32_t* blocks, int32_t* tiles) {
+  CHECK(validate_shape(nullptr, M, N, 8, P));
+  if (order < 0 || order > 2) return fail(nullptr, ENTWINE_EINVAL, "unknown order");
+  if (BM <= 0 || BN <= 0 || BM % ENTWINE_TILE || BN % ENTWINE_TILE || (M / P) % BM || N % BN)
+    return fail(nullptr, ENTWINE_EUNSUPPORTED, "block shape does not tile the chunk");
+  const BlockGrid g = make_grid(int(M), int(N), P, BM, BN);
+  const int nb = g.MB * g.NB;
+  const int tiles_n = int(N / ENTWINE_TILE);
+  for (int p = 0; p < nb; ++p) {
+    const BlockPos b = block_of_position(order, p, g);
+    if (blocks) {
+      blocks[4 * p + 0] = b.d;
+      blocks[4 * p + 1] = b.l;
+      blocks[4 * p + 2] = b.mb;
+      blocks[4 * p + 3] = b.nb;
+    }
+  }
+  if (tiles) {
+    const int Q = tiles_per_partition(int(M), int(N), P);
+    for (int d = 0; d < P; ++d)
+      for (int t = 0; t < Q; ++t) {
+        int tr, tc;
+        tile_of_number(d, t, g, &tr, &tc);
+        tiles[2 * (tr * tiles_n + tc) + 0] = d;
+        tiles[2 * (tr * tiles_n + tc) + 1] = t;
+      }
+  }
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_consumer_tasks(int32_t dest, int32_t P, int32_t Q, int32_t x, int32_t j, int32_t* part,
+                                      int32_t* tasks, int32_t cap, int32_t* count) {
+  if (P < 1 || Q < 0 || x < 1 || j < 0 || j >= x) return fail(nullptr, ENTWINE_EINVAL, "bad consumer arguments");
+  if (dest == ENTWINE_DEST_ALL && x % P) return fail(nullptr, ENTWINE_EINVAL, "x must be a multiple of P");
+  const ConsumerSeq s = consumer_seq(dest, P, x, j);
+  int n = 0;
+  for (int t = s.first; t < Q; t += s.stride) {
+    if (tasks && n < cap) tasks[n] = t;
+    ++n;
+  }
+  if (part) *part = s.part;
+  if (count) *count = n;
+  return ENTWINE_OK;
+}
+
+}  // extern "C"

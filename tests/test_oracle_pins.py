@@ -208,3 +208,43 @@ def test_input_generator_is_seeded_and_rounded():
     assert a1.dtype == np.uint16 and np.array_equal(a1, a2)
     v = rs.bf16_to_f64(a1)
     assert 0.015 < v.std() < 0.025
+
+
+# ---------------------------------------------------------- reducer arithmetic
+def test_rne_encoder_fixed_cases():
+    cases = {1.0: 0x3F80, -2.0: 0xC000, 1.0 + 2.0 ** -8: 0x3F80,            # tie -> even (down)
+             1.0 + 3 * 2.0 ** -8: 0x3F82,                                      # tie -> even (up)
+             1.0 + 2.0 ** -8 + 2.0 ** -20: 0x3F81, float("inf"): 0x7F80, 0.0: 0x0000,
+             (2 - 2.0 ** -7) * 2.0 ** 127: 0x7F7F,                             # largest finite
+             (2 - 2.0 ** -8) * 2.0 ** 127: 0x7F80}                             # tie above it -> inf
+    got = rs.f32_to_bf16_rne_bits(np.array(list(cases), dtype=np.float32))
+    assert got.tolist() == list(cases.values())
+    assert np.isnan(rs.bf16_to_f64(rs.f32_to_bf16_rne_bits(np.array([np.nan], np.float32))))[0]
+
+
+def test_rne_encoder_matches_torch():
+    x = np.random.default_rng(2).standard_normal(1 << 16).astype(np.float32) * 1e3
+    x[::7] = np.float32(1.0) + np.float32(2.0 ** -8) * np.arange(len(x[::7]), dtype=np.float32) % 4
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(rs.f32_to_bf16_rne_bits(x), ref)
+
+
+def test_reduce_tile_order_matters_and_is_rank_order():
+    # fp32 addition is not associative: 2^24 + 1 - 2^24 depends on the order.
+    big, one = to_bf16_bits(np.array([2.0 ** 24], np.float32)), to_bf16_bits(np.array([1.0], np.float32))
+    nbig = to_bf16_bits(np.array([-(2.0 ** 24)], np.float32))
+    got = rs.reduce_tile_f32(big, [one, nbig])          # (2^24 + 1) - 2^24 = 0 in fp32
+    assert rs.bf16_to_f64(got).tolist() == [0.0]
+    got = rs.reduce_tile_f32(big, [nbig, one])          # (2^24 - 2^24) + 1 = 1
+    assert rs.bf16_to_f64(got).tolist() == [1.0]
+
+
+def test_reduce_tile_matches_emulation_and_oracle_bound():
+    M, N, P = 32, 64, 8
+    prob = make_problem(M, N, 8, P, Dist("normal", 1.0), Dist("normal", 0.5), seed=31)
+    part = to_bf16_bits(np.random.default_rng(3).standard_normal((M, N)).astype(np.float32))
+    acc = torch.from_numpy(rs.bf16_to_f64(part)).float()
+    for pq in prob.peers:
+        acc = acc + torch.from_numpy(rs.bf16_to_f64(pq)).float()
+    ref = acc.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(rs.reduce_tile_f32(part, prob.peers), ref)
