@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of the GEMM + tile-reduce hot path on one MI355X.
+
+A step is one fused call (producer GEMM + concurrent tile reducer) for one
+rank's share of a row-parallel GEMM-ReduceScatter; successive steps cycle
+the emulated rank (destination chunk) through 0 .. P-1.  Inputs are seeded
+synthetic bf16 matrices resident in HBM before timing starts.
+
+Prints ONE JSON line: whole-job TFLOP/s (2 M N K per step), the producer
+kernel's achieved TFLOP/s against the bf16 MFMA peak (measured with HIP
+events on the producer's stream inside the timed region), the overlap
+efficiency against the uncontended producer (the paper's definition,
+Appendix C) and against GEMM-alone + reduce-alone, and the CPU oracle timed
+on the host on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E, published
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=120)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--dest", default="cycle", help="'cycle' (0..P-1 per step), 'all', or a chunk index")
+    ap.add_argument("--order", type=int, default=None)
+    ap.add_argument("--gemm-cfg", type=int, default=None)
+    ap.add_argument("--x", type=int, default=None, help="reducer workgroups (communication budget)")
+    ap.add_argument("--b", type=int, default=None, help="reducer threads per workgroup")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-legs", action="store_true", help="skip the gemm-only / reduce-only / sequential legs")
+    ap.add_argument("--only", default=None, choices=["fused", "gemm", "reduce", "seq"],
+                    help="time just one mode (for profiler runs)")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (one rank's share of the "
+              "GEMM-ReduceScatter, peers emulated in HBM); --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from paper_2609_11562_amd import entwine as E
+    from paper_2609_11562_amd.inputs import bits_to_torch
+    from paper_2609_11562_amd.tuning import tuned_config
+    from paper_2609_11562_amd.workloads import BENCH_WORKLOAD, WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    E.lib()  # fail loudly if the HIP library is missing
+
+    w = WORKLOADS[args.workload or BENCH_WORKLOAD]
+    M, N, K, P = w.M, w.N, w.K, w.P
+    t_gen = time.perf_counter()
+    prob = w.problem()
+    A = bits_to_torch(prob.A).cuda()
+    B = bits_to_torch(prob.B).cuda()
+    peers = [bits_to_torch(p).cuda() for p in prob.peers]
+    t_gen = time.perf_counter() - t_gen
+
+    dest_mode = args.dest
+    all_chunks = dest_mode == "all"
+    tuned = tuned_config(w.name, "all" if all_chunks else "rank")
+    kw = dict(tuned)
+    for k, v in (("order", args.order), ("gemm_cfg", args.gemm_cfg), ("reduce_wgs", args.x),
+                 ("reduce_threads", args.b)):
+        if v is not None:
+            kw[k] = v
+    cfg = E.Config.make(**kw, record_timing=1)
+
+    def dest_of(i):
+        if all_chunks:
+            return E.DEST_ALL
+        if dest_mode == "cycle":
+            return i % P
+        return int(dest_mode)
+
+    ctx = E.Context(M, N, K, P)
+    partial = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    outs = {d: torch.empty(ctx.out_rows(d), N, dtype=torch.bfloat16, device="cuda")
+            for d in ([E.DEST_ALL] if all_chunks else range(P))}
+    gs = torch.cuda.current_stream()
+    rs = torch.cuda.Stream()
+
+    def step(i, mode="fused"):
+        d = dest_of(i)
+        if mode == "fused":
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
+        elif mode == "seq":
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=gs)
+        elif mode == "gemm":
+            ctx.gemm_only(A, B, partial=partial, cfg=cfg, stream=gs)
+        else:
+            ctx.reduce_only(partial, peers, d, out=outs[d], cfg=cfg, stream=gs)
+
+    def timed(mode, steps, warmup):
+        for i in range(warmup):
+            step(i, mode)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(i, mode)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        st = ctx.query_status()
+        if st[0] != E.OK:
+            raise SystemExit(f"bench.py: reducer reported status {st}")
+        n = min(steps, 255)
+        per = [ctx.last_timing(b) for b in range(n)]
+        return wall, per
+
+    main_mode = args.only or "fused"
+    ms_per_step, per = timed(main_mode, args.steps, args.warmup)
+    g_ms = [p[0] for p in per if p[0] > 0]
+    r_ms = [p[1] for p in per if p[1] > 0]
+    e_ms = [p[2] for p in per if p[2] > 0]
+
+    flops = 2.0 * M * N * K
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    mean_g = statistics.fmean(g_ms) if g_ms else None
+    achieved = flops / (mean_g * 1e-3) / 1e12 if mean_g else None
+
+    legs = {}
+    if not args.no_legs and args.only is None:
+        n_leg, w_leg = max(20, min(args.steps, 100)), 10
+        _, p_g = timed("gemm", n_leg, w_leg)
+        _, p_r = timed("reduce", n_leg, w_leg)
+        seq_wall, p_s = timed("seq", n_leg, w_leg)
+        _, p_f = timed("fused", n_leg, w_leg)
+        med = statistics.median
+        T_G = med([p[0] for p in p_g])
+        T_R = med([p[1] for p in p_r])
+        T_seq = med([p[2] for p in p_s])
+        T_fused = med([p[2] for p in p_f])
+        tails = [max(0.0, p[1] - p[0]) for p in p_f]
+        rbytes = 2.0 * ((M if all_chunks else M // P) * N * (P + 1))
+        legs = {
+            "T_gemm_alone_ms": T_G, "T_reduce_alone_ms": T_R, "T_sequential_ms": T_seq,
+            "T_fused_ms": T_fused, "gemm_in_fused_ms": med([p[0] for p in p_f]),
+            "tail_ms": med(tails),
+            "eta_fused": T_G / T_fused,                 # uncontended producer / end-to-end
+            "eta_vs_unfused": (T_G + T_R) / T_fused,    # (GEMM alone + reduce alone) / fused
+            "speedup_vs_sequential": T_seq / T_fused,
+            "reducer_alone_GBps": rbytes / (T_R * 1e-3) / 1e9,
+            "B_req_GBps": ((P - 1) / P) * M * N * 2 / (med([p[0] for p in p_f]) * 1e-3) / 1e9,
+            "gemm_alone_tflops": flops / (T_G * 1e-3) / 1e12,
+        }
+
+    copy = None
+    if args.copy_calib_mib:
+        n = args.copy_calib_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        copy = {"bytes_read": n * 4, "bytes_written": n * 4}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(prob, w, outs, all_chunks, dest_of)
+
+    ctx.close()
+    rec = {
+        "metric": "GEMM+tile-reduce TFLOP/s (bf16, 1 GPU) and overlap efficiency vs unfused",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded bf16 A, B ~ N(0, 0.02); peer partials with matching variance)",
+        "config": {"workload": w.name, "M": M, "N": N, "K": K, "P": P,
+                   "dest": "all" if all_chunks else dest_mode, "mode": main_mode,
+                   "order": cfg.order, "gemm_cfg": cfg.gemm_cfg, "reduce_wgs": cfg.reduce_wgs,
+                   "reduce_threads": cfg.reduce_threads},
+        "roofline": {"bound": "mfma", "kernel": "gemm_producer",
+                     "achieved": round(achieved, 2) if achieved else None,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
+                     "traffic": None,
+                     "gemm_kernel_mean_ms": round(mean_g, 5) if mean_g else None},
+        "cpu_baseline": cpu,
+        "overlap": legs,
+        "input_gen_s": round(t_gen, 2),
+    }
+    if copy:
+        rec["copy_calibration"] = copy
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(prob, w, outs, all_chunks, dest_of):
+    """The CPU oracle, as it stands, timed on the host: every chunk of the
+    workload (the whole job), repeated until about 10 s have elapsed or three
+    runs are done.  Also compares the GPU's last outputs on sampled rows."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
+                      default=1)
+    except Exception:  # noqa: BLE001
+        threads = None
+    runs = []
+    t_end = time.perf_counter() + 10.0
+    while len(runs) < 3 and (not runs or time.perf_counter() < t_end):
+        t0 = time.perf_counter()
+        C = oracle.local_partial(prob.A, prob.B)
+        for d in range(w.P):
+            oracle.reduce_chunk(C, prob.peers, w.P, d)
+        runs.append(time.perf_counter() - t0)
+        del C
+    t = statistics.median(runs)
+    # spot check of the GPU outputs left by the timed loop
+    import torch
+    o = outs[-1 if all_chunks else 0].view(torch.int16).cpu().numpy().view(np.uint16)
+    rows = np.arange(0, o.shape[0], max(1, o.shape[0] // 16))   # chunk 0 rows are global rows
+    ref = oracle.output_rows(prob.A, prob.B, prob.peers, rows)
+    got = oracle.bf16_to_f64(o[rows])
+    bound = oracle.error_bound_rows(prob.A, prob.B, prob.peers, rows)
+    return {"value": round(w.flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle", "seconds_per_job": round(t, 3), "runs": len(runs),
+            "sample": f"whole job ({w.name}, all {w.P} chunks, fp64 numpy), median of {len(runs)} runs",
+            "gpu_spot_check": {"rows": int(len(rows)), "max_abs_err": float(np.abs(got - ref).max()),
+                               "within_bound": bool(np.all(np.abs(got - ref) <= bound)),
+                               "paper_gate": bool(np.all(oracle.paper_gate(got, ref)))}}
+
+
+if __name__ == "__main__":
+    main()

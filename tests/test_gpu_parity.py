@@ -1,0 +1,244 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Floating-point results must pass both the paper's gate
+(|err| <= 0.1 + 0.05 |ref|) and the elementwise rounding bound of a
+bf16-in / fp32-accumulate / bf16-partial / fp32-reduce / bf16-out path.
+Integer-valued inputs small enough to be exact at every step must match
+bit for bit.  Full-size workloads are checked on sampled rows (every column
+of each sampled row, so every column tile is covered)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_11562_amd import entwine as E
+from paper_2609_11562_amd.inputs import Dist, bits_to_torch, make_problem
+from paper_2609_11562_amd.workloads import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(bits):
+    return bits_to_torch(bits).cuda()
+
+
+def host_bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def upload(prob):
+    return dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
+
+
+def out_global_rows(M, P, dest):
+    return np.arange(M) if dest == E.DEST_ALL else np.arange(dest * (M // P), (dest + 1) * (M // P))
+
+
+def check_rows(prob, got_bits, grow, local_rows=None):
+    """got_bits: GPU output rows (bf16 bits) for global rows `grow`."""
+    ref = oracle.output_rows(prob.A, prob.B, prob.peers, grow)
+    bound = oracle.error_bound_rows(prob.A, prob.B, prob.peers, grow)
+    got = oracle.bf16_to_f64(got_bits)
+    assert not np.isnan(got).any(), "NaN in output"
+    gate = oracle.paper_gate(got, ref)
+    err = np.abs(got - ref)
+    assert gate.all(), f"paper gate fails at {np.argwhere(~gate)[:5].tolist()}"
+    bad = err > bound
+    assert not bad.any(), (f"rounding bound exceeded at {np.argwhere(bad)[:5].tolist()}, "
+                           f"max err {err.max():.3g}")
+
+
+def run(ctx, A, B, peers, dest, cfg=None, fused=True, out=None, partial=None):
+    rs = torch.cuda.Stream() if fused else None
+    o = ctx.gemm_rs(A, B, peers, dest, out=out, partial=partial, cfg=cfg, reduce_stream=rs)
+    st, tile, src = ctx.query_status()
+    assert st == E.OK, f"status {st} tile {tile} src {src}"
+    return o
+
+
+# --------------------------------------------------------------- small case
+@pytest.fixture(scope="module")
+def tiny():
+    w = WORKLOADS["tiny_512x256x1024_p2"]
+    prob = w.problem()
+    ctx = E.Context(w.M, w.N, w.K, w.P)
+    yield w, prob, ctx, upload(prob)
+    ctx.close()
+
+
+@pytest.mark.parametrize("dest", [0, 1, E.DEST_ALL])
+@pytest.mark.parametrize("order", [E.ORDER_INTERLEAVED, E.ORDER_ROW_MAJOR, E.ORDER_M_MAJOR])
+def test_tiny_matches_oracle(tiny, dest, order):
+    w, prob, ctx, (A, B, peers) = tiny
+    print(f"[tiny] dest={dest} order={order}", flush=True)
+    o = run(ctx, A, B, peers, dest, E.Config.make(order=order))
+    torch.cuda.synchronize()
+    check_rows(prob, host_bits(o), out_global_rows(w.M, w.P, dest))
+
+
+@pytest.mark.parametrize("gemm_cfg", [0, 1, 2, 3])
+def test_tiny_every_block_shape(tiny, gemm_cfg):
+    w, prob, ctx, (A, B, peers) = tiny
+    print(f"[tiny] gemm_cfg={gemm_cfg}", flush=True)
+    o = run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(gemm_cfg=gemm_cfg, reduce_wgs=4))
+    torch.cuda.synchronize()
+    check_rows(prob, host_bits(o), np.arange(w.M))
+
+
+# --------------------------------------------------------------- exact integer cases
+@pytest.mark.parametrize("M,N,K,P,a,pk", [(512, 256, 96, 4, 1, 16), (1024, 384, 128, 8, 1, 16),
+                                          (256, 128, 16, 2, 2, 16), (2048, 512, 40, 8, 1, 8),
+                                          (128, 128, 8, 1, 1, 0)])
+def test_integer_inputs_bit_exact(M, N, K, P, a, pk):
+    print(f"[int] M={M} N={N} K={K} P={P}", flush=True)
+    prob = make_problem(M, N, K, P, Dist("int", a), Dist("int", max(pk, 1)), seed=M + K)
+    A, B, peers = upload(prob)
+    ref = oracle.gemm_reduce_scatter(prob.A, prob.B, prob.peers, P, E.DEST_ALL)
+    with E.Context(M, N, K, P) as ctx:
+        for cfg in (0, 3):
+            if (M // P) % E.GEMM_SHAPES[cfg][0] or N % E.GEMM_SHAPES[cfg][1]:
+                continue
+            o = run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(gemm_cfg=cfg))
+            torch.cuda.synchronize()
+            got = oracle.bf16_to_f64(host_bits(o))
+            assert np.array_equal(got, ref), f"max diff {np.abs(got - ref).max()}"
+
+
+# --------------------------------------------------------------- K tails, odd shapes
+@pytest.mark.parametrize("M,N,K,P", [(256, 128, 8, 2), (512, 256, 40, 4), (1024, 512, 1376, 8),
+                                     (768, 384, 200, 3), (1280, 640, 72, 5)])
+def test_k_tail_and_odd_p(M, N, K, P):
+    print(f"[tail] M={M} N={N} K={K} P={P}", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 4e-4 * K ** 0.5), seed=K)
+    A, B, peers = upload(prob)
+    with E.Context(M, N, K, P) as ctx:
+        for dest in (0, P - 1, E.DEST_ALL):
+            o = run(ctx, A, B, peers, dest, E.Config.make(gemm_cfg=E.GEMM_128x128))
+            torch.cuda.synchronize()
+            check_rows(prob, host_bits(o), out_global_rows(M, P, dest))
+
+
+# --------------------------------------------------------------- invariants (bitwise)
+def test_results_independent_of_order_budget_threads_and_mode():
+    M, N, K, P = 2048, 1024, 520, 4
+    print("[invariants]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 4e-4 * K ** 0.5), seed=99)
+    A, B, peers = upload(prob)
+    with E.Context(M, N, K, P) as ctx:
+        base = host_bits(run(ctx, A, B, peers, E.DEST_ALL))
+        torch.cuda.synchronize()
+        check_rows(prob, base[::37], np.arange(M)[::37])
+        variants = [dict(order=o) for o in (1, 2)] + [dict(gemm_cfg=c) for c in (1, 2, 3)] + \
+                   [dict(reduce_wgs=x) for x in (4, 8, 32, 64)] + \
+                   [dict(reduce_threads=b) for b in (128, 512)]
+        for kw in variants:
+            o = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(**kw)))
+            assert np.array_equal(o, base), kw
+        seq = host_bits(run(ctx, A, B, peers, E.DEST_ALL, fused=False))
+        assert np.array_equal(seq, base), "sequential differs from fused"
+        parts = [host_bits(run(ctx, A, B, peers, d, E.Config.make(reduce_wgs=x)))
+                 for d, x in zip(range(P), (1, 3, 16, 64))]
+        assert np.array_equal(np.concatenate(parts, axis=0), base), "chunks differ from all-chunk output"
+
+
+def test_reducer_is_exact_on_given_partial():
+    """reduce_only on a known partial equals the fp32 rank-order sum rounded
+    to bf16, bit for bit; gemm_only's partial stays within the GEMM bound."""
+    M, N, K, P = 1024, 512, 256, 8
+    print("[reduce_only]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.01), seed=5)
+    A, B, peers = upload(prob)
+    with E.Context(M, N, K, P) as ctx:
+        partial = ctx.gemm_only(A, B)
+        torch.cuda.synchronize()
+        pbits = host_bits(partial)
+        C = oracle.local_partial(prob.A, prob.B)
+        absab = np.abs(oracle.bf16_to_f64(prob.A)) @ np.abs(oracle.bf16_to_f64(prob.B))
+        err = np.abs(oracle.bf16_to_f64(pbits) - C)
+        assert np.all(err <= 2 * 2.0 ** -8 * np.abs(C) + 2 * 2.0 ** -24 * K * absab)
+        for dest in (3, E.DEST_ALL):
+            o = ctx.reduce_only(partial, peers, dest)
+            assert ctx.query_status()[0] == E.OK
+            rows = out_global_rows(M, P, dest)
+            want = oracle.reduce_scatter.reduce_tile_f32(pbits[rows], [p[rows] for p in prob.peers])
+            assert np.array_equal(host_bits(o), want)
+
+
+# --------------------------------------------------------------- protocol
+def test_withheld_peer_times_out_then_recovers(tiny):
+    w, prob, ctx, (A, B, peers) = tiny
+    print("[timeout]", flush=True)
+    cfg = E.Config.make(withhold_peer=0, timeout_us=20000, reduce_wgs=2)
+    ctx.gemm_rs(A, B, peers, 1, cfg=cfg, reduce_stream=torch.cuda.Stream())
+    st, tile, src = ctx.query_status()
+    assert st == E.ETIMEOUT and src == 0 and 0 <= tile < (w.M // 128) * (w.N // 128)
+    o = run(ctx, A, B, peers, 1)
+    torch.cuda.synchronize()
+    check_rows(prob, host_bits(o), out_global_rows(w.M, w.P, 1))
+
+
+def test_poisoned_buffers_never_leak_across_repeated_calls():
+    """Partial and output are NaN-poisoned before every call and two input
+    sets alternate, so a read before publication, a stale cache line from an
+    earlier call or a missed tile shows up as NaN or as the other set's value."""
+    M, N, K, P = 2048, 2048, 256, 8
+    print("[poison]", flush=True)
+    probs = [make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.01), seed=s) for s in (1, 2)]
+    ups = [upload(p) for p in probs]
+    want = []
+    nan = torch.tensor(0x7FC0, dtype=torch.int16).view(torch.bfloat16)
+    partial = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty(M // P, N, dtype=torch.bfloat16, device="cuda")
+    rs = torch.cuda.Stream()
+    with E.Context(M, N, K, P) as ctx:
+        for i in range(24):
+            A, B, peers = ups[i % 2]
+            partial.fill_(nan)
+            out.fill_(nan)
+            ctx.gemm_rs(A, B, peers, 5, out=out, partial=partial, reduce_stream=rs,
+                        cfg=E.Config.make(reduce_wgs=8 + i))
+            got = host_bits(out)
+            if i < 2:
+                check_rows(probs[i], got, out_global_rows(M, P, 5))
+                want.append(got)
+            else:
+                assert np.array_equal(got, want[i % 2]), f"call {i}"
+        assert ctx.query_status()[0] == E.OK
+
+
+def test_bad_arguments_are_rejected(tiny):
+    w, prob, ctx, (A, B, peers) = tiny
+    with pytest.raises(E.EntwineError) as ei:
+        ctx.gemm_rs(A, B, peers, 5)
+    assert ei.value.status == E.EINVAL
+    with pytest.raises(ValueError):
+        ctx.gemm_rs(A[:, :128], B, peers, 0)
+    with pytest.raises(ValueError):
+        ctx.gemm_rs(A, B, peers[:0], 0)
+
+
+# --------------------------------------------------------------- full sizes
+def sample_rows(M, P, dest, n=24, seed=0):
+    rows = out_global_rows(M, P, dest)
+    rng = np.random.default_rng(seed)
+    pick = set(rng.choice(rows, size=min(n, len(rows)), replace=False).tolist())
+    pick |= {int(rows[0]), int(rows[-1]), int(rows[len(rows) // 2]), int(rows[127 % len(rows)])}
+    return np.array(sorted(pick))
+
+
+@pytest.mark.parametrize("name", ["llama7b_mlp_down_tp8", "llama70b_attn_out_tp8", "llama70b_mlp_down_tp8",
+                                  "sweep_8192x512x8192_p2", "sweep_8192x2048x8192_p4"])
+def test_full_size_workloads_on_sampled_rows(name):
+    w = WORKLOADS[name]
+    print(f"[full] {name}", flush=True)
+    prob = w.problem()
+    A, B, peers = upload(prob)
+    with E.Context(w.M, w.N, w.K, w.P) as ctx:
+        for dest in (0, w.P - 1, E.DEST_ALL):
+            o = run(ctx, A, B, peers, dest, E.Config.make(reduce_wgs=16))
+            torch.cuda.synchronize()
+            grow = sample_rows(w.M, w.P, dest, seed=dest + 1)
+            local = grow - (0 if dest == E.DEST_ALL else dest * (w.M // w.P))
+            check_rows(prob, host_bits(o[torch.as_tensor(local, device="cuda")]), grow)
+    del A, B, peers
+    torch.cuda.empty_cache()
