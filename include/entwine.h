@@ -85,7 +85,9 @@ typedef struct {
   int32_t withhold_peer;  /* test hook: peer q whose flags are not published
                              this call (-1 = none); forces a timeout */
   int32_t record_timing;  /* 1 = record events for entwine_last_timing() */
-  int32_t reserved;
+  int32_t group_m;        /* block order inside a partition: 1 = N-major (the
+                             paper's), g > 1 = XCD-striped walk in groups of g
+                             block rows (L2 reuse); 0 = default (4) */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */
@@ -149,12 +151,14 @@ entwine_status entwine_validate(int64_t M, int64_t N, int64_t K, int32_t P, int3
                                 const entwine_config* cfg);
 
 /* Host-only export of the traversal (Equation 1 and the comparison orders)
- * for a BM x BN block grid.  blocks: (M/BM)(N/BN) x 4 int32, per logical
- * position p: (d, l, block row, block col).  tiles: (M/128)(N/128) x 2
- * int32, per global tile in row-major tile order: (partition d, tile number t
- * inside d in producer order).  Either may be NULL. */
+ * for a BM x BN block grid and a within-partition walk group_m (as in
+ * entwine_config, but 0 = N-major here).  blocks: (M/BM)(N/BN) x 4 int32,
+ * per logical position p: (d, l, block row, block col).  tiles:
+ * (M/128)(N/128) x 2 int32, per global tile in row-major tile order:
+ * (partition d, tile number t inside d in producer order).  Either may be
+ * NULL. */
 entwine_status entwine_tile_schedule(int32_t order, int64_t M, int64_t N, int32_t P, int32_t BM,
-                                     int32_t BN, int32_t* blocks, int32_t* tiles);
+                                     int32_t BN, int32_t group_m, int32_t* blocks, int32_t* tiles);
 
 /* Host-only export of the consumer assignment (Section 3.1, "Matching task
  * order"): the partition and tile numbers processed, in order, by reducer

@@ -22,6 +22,15 @@ Terms (paper, Section 3.1):
   1 x 2 example: block p=1 yields t0 and t1).
 * Consumer block j of x processes tiles j, j+x, j+2x, ... below Q, where Q is
   the partition's tile count ("Matching task order").
+
+The paper fixes the walk inside a partition to N-major.  The build also has
+an L2-friendly walk (group_m > 1) that is not from the paper: with workgroup
+b running on XCD b mod 8, partition d is served by G = 8 / P XCDs (P | 8) and
+index l goes to stripe l mod G (column stripes when they divide the block
+columns, else row stripes, else one stripe); each stripe is walked in groups
+of group_m block rows (the largest divisor of the stripe's rows not above
+group_m), M fastest inside a group, then the stripes are interleaved.  It is
+restated here from that description, independently of the library.
 """
 from __future__ import annotations
 
@@ -31,27 +40,51 @@ M_MAJOR = 2
 TILE = 128
 
 
-def producer_block(order: int, p: int, M: int, N: int, P: int, BM: int, BN: int):
+def partition_walk(RB: int, NB: int, P: int, group_m: int = 1, xcds: int = 8):
+    """Block coordinates (row, col) inside one partition (RB x NB blocks), in
+    the order the partition's blocks are produced and consumed."""
+    if group_m <= 1:
+        return [(l // NB, l % NB) for l in range(RB * NB)]      # N-major (paper)
+    G = xcds // P if (P <= xcds and xcds % P == 0) else 1
+    if NB % G == 0:
+        stripes = [(0, RB, s * (NB // G), NB // G) for s in range(G)]
+    elif RB % G == 0:
+        stripes = [(s * (RB // G), RB // G, 0, NB) for s in range(G)]
+    else:
+        G, stripes = 1, [(0, RB, 0, NB)]
+    walks = []
+    for r0, nr, c0, nc in stripes:
+        gm = max(k for k in range(1, min(group_m, nr) + 1) if nr % k == 0)
+        walk = []
+        for grp in range(nr // gm):
+            for c in range(nc):
+                for r in range(gm):
+                    walk.append((r0 + grp * gm + r, c0 + c))
+        walks.append(walk)
+    return [walks[l % G][l // G] for l in range(RB * NB)]
+
+
+def producer_block(order: int, p: int, M: int, N: int, P: int, BM: int, BN: int, group_m: int = 1):
     """Map logical position p to (d, l, mb, nb): destination partition,
-    index inside the partition (N-major), and the block's row / column index
-    in the M/BM x N/BN block grid."""
+    index inside the partition (its walk), and the block's row / column
+    index in the M/BM x N/BN block grid."""
     MB, NB = M // BM, N // BN
     rows_per_part = (M // P) // BM          # block rows in one partition
     if not 0 <= p < MB * NB:
         raise ValueError("position out of range")
+    walk = partition_walk(rows_per_part, NB, P, group_m)
     if order == INTERLEAVED:
         d = p % P                            # Equation 1
         l = p // P
-        mb = d * rows_per_part + l // NB
-        nb = l % NB
-    elif order == ROW_MAJOR:
-        mb, nb = p // NB, p % NB
+        r, c = walk[l]
+        mb, nb = d * rows_per_part + r, c
+    elif order in (ROW_MAJOR, M_MAJOR):
+        if order == ROW_MAJOR:
+            mb, nb = p // NB, p % NB
+        else:
+            mb, nb = p % MB, p // MB
         d = mb // rows_per_part
-        l = (mb % rows_per_part) * NB + nb
-    elif order == M_MAJOR:
-        mb, nb = p % MB, p // MB
-        d = mb // rows_per_part
-        l = (mb % rows_per_part) * NB + nb
+        l = walk.index((mb % rows_per_part, nb))
     else:
         raise ValueError("unknown order")
     return d, l, mb, nb
@@ -73,12 +106,12 @@ def partition_tile_number(l: int, i: int, BM: int, BN: int) -> int:
     return l * c + i
 
 
-def full_schedule(order: int, M: int, N: int, P: int, BM: int, BN: int):
+def full_schedule(order: int, M: int, N: int, P: int, BM: int, BN: int, group_m: int = 1):
     """Per logical position: (d, l, mb, nb, [(t, tile_row, tile_col), ...])."""
     nblocks = (M // BM) * (N // BN)
     sched = []
     for p in range(nblocks):
-        d, l, mb, nb = producer_block(order, p, M, N, P, BM, BN)
+        d, l, mb, nb = producer_block(order, p, M, N, P, BM, BN, group_m)
         tiles = [(partition_tile_number(l, i, BM, BN), tr, tc)
                  for i, (tr, tc) in enumerate(block_tiles(mb, nb, BM, BN))]
         sched.append((d, l, mb, nb, tiles))

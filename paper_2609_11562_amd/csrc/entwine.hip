@@ -51,6 +51,7 @@ struct entwine_ctx {
   int* peer_flags = nullptr;   // (P-1) x ntiles
   int* status = nullptr;       // {code, tile, src, pad}
   uint16_t* scratch = nullptr; // M x N partial when the caller passes none
+  uint16_t* zeros = nullptr;   // zero page read by the producer for the K tail
   uint32_t epoch = 0;
   uint64_t ticks_per_us = 100;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
@@ -100,7 +101,7 @@ int default_gemm_cfg(int64_t M, int64_t N, int P) {
 }
 
 struct Resolved {
-  int order, gemm_cfg, BM, BN, x, threads, withhold, timing;
+  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m;
   uint64_t timeout_us;
 };
 
@@ -118,6 +119,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.reduce_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "reduce_wgs must be >= 0");
   if (c.timeout_us < 0) return fail(ctx, ENTWINE_EINVAL, "timeout_us must be >= 0");
   if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
+  if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -140,6 +142,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->withhold = c.withhold_peer;
   r->timing = c.record_timing;
   r->timeout_us = c.timeout_us ? uint64_t(c.timeout_us) : 2000000ull;
+  r->group_m = c.group_m ? c.group_m : 4;
   return ENTWINE_OK;
 }
 
@@ -164,14 +167,6 @@ GemmKernel gemm_kernel(int cfg) {
     case 1: return gemm_producer<256, 128>;
     case 2: return gemm_producer<128, 256>;
     default: return gemm_producer<128, 128>;
-  }
-}
-int gemm_lds_bytes(int cfg) {
-  switch (cfg) {
-    case 0: return GemmShape<256, 256>::LDS_BYTES;
-    case 1: return GemmShape<256, 128>::LDS_BYTES;
-    case 2: return GemmShape<128, 256>::LDS_BYTES;
-    default: return GemmShape<128, 128>::LDS_BYTES;
   }
 }
 
@@ -226,6 +221,7 @@ entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, i
   g.A = static_cast<const uint16_t*>(A);
   g.B = static_cast<const uint16_t*>(B);
   g.C = static_cast<uint16_t*>(C);
+  g.zeros = ctx->zeros;
   g.lda = lda;
   g.ldb = ldb;
   g.ldc = ldc;
@@ -234,10 +230,11 @@ entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, i
   g.K = int(ctx->K);
   g.P = ctx->P;
   g.order = r.order;
+  g.group_m = r.group_m;
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
   const int nblocks = int((ctx->M / r.BM) * (ctx->N / r.BN));
-  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(nblocks), dim3(256), gemm_lds_bytes(r.gemm_cfg), s, g);
+  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(nblocks), dim3(256), 0, s, g);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }
@@ -268,6 +265,7 @@ entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* pa
   ra.x = r.x;
   ra.BM = r.BM;
   ra.BN = r.BN;
+  ra.group_m = r.group_m;
   ra.flags = ctx->flags;
   ra.peer_flags = ctx->peer_flags;
   ra.epoch = epoch;
@@ -298,7 +296,7 @@ void entwine_config_default(entwine_config* cfg) {
   cfg->timeout_us = 0;
   cfg->withhold_peer = -1;
   cfg->record_timing = 0;
-  cfg->reserved = 0;
+  cfg->group_m = 0;
 }
 
 int32_t entwine_abi_version(void) { return ENTWINE_ABI_VERSION; }
@@ -353,11 +351,11 @@ entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, 
   const size_t fbytes = size_t(c->ntiles) * sizeof(int);
   if (hipMalloc(&c->flags, fbytes) != hipSuccess ||
       hipMalloc(&c->peer_flags, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
-      hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess)
+      hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess || hipMalloc(&c->zeros, 256) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_ENOMEM, "flag allocation failed"));
   if (hipMemset(c->flags, 0, fbytes) != hipSuccess ||
       hipMemset(c->peer_flags, 0, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
-      hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess)
+      hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess || hipMemset(c->zeros, 0, 256) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_EHIP, "flag initialisation failed"));
   if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
@@ -366,10 +364,6 @@ entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, 
     if (hipEventCreate(&s.start) != hipSuccess || hipEventCreate(&s.gemm_end) != hipSuccess ||
         hipEventCreate(&s.red_end) != hipSuccess)
       return bail(fail(nullptr, ENTWINE_EHIP, "event creation failed"));
-  for (int cfg = 0; cfg < ENTWINE_GEMM_NUM_CFGS; ++cfg)
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel(cfg)),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes(cfg)) != hipSuccess)
-      return bail(fail(nullptr, ENTWINE_EHIP, "LDS size attribute failed"));
   if (hipDeviceSynchronize() != hipSuccess) return bail(fail(nullptr, ENTWINE_EHIP, "initial sync failed"));
   *out = c;
   return ENTWINE_OK;
@@ -383,6 +377,7 @@ entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
   if (ctx->peer_flags) (void)hipFree(ctx->peer_flags);
   if (ctx->status) (void)hipFree(ctx->status);
   if (ctx->scratch) (void)hipFree(ctx->scratch);
+  if (ctx->zeros) (void)hipFree(ctx->zeros);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   for (auto& s : ctx->ring) {
@@ -530,12 +525,13 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
 }
 
 entwine_status entwine_tile_schedule(int32_t order, int64_t M, int64_t N, int32_t P, int32_t BM, int32_t BN,
-                                     int32_t* blocks, int32_t* tiles) {
+                                     int32_t group_m, int32_t* blocks, int32_t* tiles) {
   CHECK(validate_shape(nullptr, M, N, 8, P));
   if (order < 0 || order > 2) return fail(nullptr, ENTWINE_EINVAL, "unknown order");
   if (BM <= 0 || BN <= 0 || BM % ENTWINE_TILE || BN % ENTWINE_TILE || (M / P) % BM || N % BN)
     return fail(nullptr, ENTWINE_EUNSUPPORTED, "block shape does not tile the chunk");
-  const BlockGrid g = make_grid(int(M), int(N), P, BM, BN);
+  if (group_m < 0 || group_m > 64) return fail(nullptr, ENTWINE_EINVAL, "group_m outside [0, 64]");
+  const BlockGrid g = make_grid(int(M), int(N), P, BM, BN, group_m);
   const int nb = g.MB * g.NB;
   const int tiles_n = int(N / ENTWINE_TILE);
   for (int p = 0; p < nb; ++p) {

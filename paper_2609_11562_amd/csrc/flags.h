@@ -29,6 +29,14 @@ __device__ __forceinline__ void publish_release(int* flag, uint32_t epoch) {
   __hip_atomic_store(flag, static_cast<int>(epoch), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Release fence once, then relaxed stores: one L2 write-back covers every
+// flag a producer block publishes.
+__device__ __forceinline__ void release_fence() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+
+__device__ __forceinline__ void publish_relaxed(int* flag, uint32_t epoch) {
+  __hip_atomic_store(flag, static_cast<int>(epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ int poll_relaxed(const int* flag) {
   return __hip_atomic_load(const_cast<int*>(flag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

@@ -4,18 +4,30 @@
 //
 // One workgroup computes a BM x BN block of C = A B (A: M x K, B: K x N, both
 // row-major bf16) with 4 waves in a 2 x 2 arrangement; each wave owns a
-// (BM/2) x (BN/2) sub-block as 32 x 32 MFMA accumulators
-// (v_mfma_f32_32x32x16_bf16, fp32 accumulate).
+// (BM/2) x (BN/2) sub-block held as 32 x 32 MFMA accumulators
+// (v_mfma_f32_32x32x16_bf16: fp32 accumulate, 16 K per instruction).
 //
-// K is walked in slabs of 64.  Each slab of A (BM x 64) and B (64 x BN) is
-// staged through LDS, double-buffered: the global loads of slab k+1 are in
-// flight while slab k feeds the MFMAs.  MFMA operands want K contiguous per
-// lane, so A is stored as is and B is stored transposed ([n][k]); the
-// transpose is done in registers, one 8 x 8 block per thread.  LDS rows are
-// 128 bytes with their 16-byte chunks XOR-swizzled so that both the staging
-// writes and the operand reads are free of bank conflicts.
-//
-// The K tail (K % 64) is zero-filled (K % 8 == 0 keeps 16-byte rows whole).
+// Data path per K-slab of 32:
+//  * global -> LDS with direct-to-LDS loads (global_load_lds_dwordx4): each
+//    instruction moves 64 lanes x 16 bytes into 1 KB of contiguous LDS, no
+//    registers involved.  A slab lives in one of 4 LDS stages; the loads for
+//    slab k+3 are issued while slab k is being multiplied.
+//  * LDS layouts are chosen for conflict-free operand reads, and realised by
+//    permuting which global 16-byte chunk each lane fetches:
+//      A stage: [BM rows][32 k] (64-byte rows), chunk c of row r stored at
+//               chunk c ^ ((r >> 2) & 3);
+//      B stage: [32 k][BN n] (row-major, as in memory), chunk c of row k
+//               stored at chunk c ^ (4 (k & 3)).
+//  * A operands: one ds_read_b128 per 32 x 16 fragment (8 consecutive k per
+//    lane).  B operands: the MFMA wants 8 consecutive k of one column per
+//    lane, while B is row-major; gfx950's ds_read_b64_tr_b16 transposes
+//    4 x 16 blocks across each group of 16 lanes (lane i receives element
+//    i % 4 of the 8 bytes addressed by lane 4e + i / 4, for e = 0..3), so two
+//    such reads build one fragment with no register shuffles.
+//  * Operand fragments of slab k+1 are read from LDS before the MFMAs of
+//    slab k are issued (double-buffered in registers).
+// The K tail (K % 32) is handled without branches: lanes whose 16-byte chunk
+// lies beyond K fetch from a zero page instead.
 //
 // Epilogue: the MFMA is issued with the B fragment as its first operand, so
 // each lane ends up holding 4 consecutive N values of one output row; they
@@ -26,47 +38,71 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "flags.h"
 #include "tile_order.h"
 
 namespace entwine {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 struct GemmArgs {
   const uint16_t* A;
   const uint16_t* B;
   uint16_t* C;
+  const uint16_t* zeros;  // >= 16 readable bytes of zeros (K-tail fill)
   int64_t lda, ldb, ldc;
-  int M, N, K, P, order;
-  int* flags;       // one per global 128 x 128 tile, row-major; null = no publish
+  int M, N, K, P, order, group_m;
+  int* flags;             // one per global 128 x 128 tile, row-major; null = no publish
   uint32_t epoch;
 };
 
 template <int BM_, int BN_>
 struct GemmShape {
   static constexpr int BM = BM_, BN = BN_;
-  static constexpr int BK = 64;
+  static constexpr int BK = 32;
   static constexpr int THREADS = 256;
+  static constexpr int STAGES = 4;
   static constexpr int WM = BM / 2, WN = BN / 2;     // wave sub-block
   static constexpr int FM = WM / 32, FN = WN / 32;   // 32 x 32 MFMA blocks per wave
-  static constexpr int A_BYTES = BM * BK * 2;
-  static constexpr int B_BYTES = BN * BK * 2;
-  static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int LDS_BYTES = 2 * STAGE;
-  static constexpr int A_CHUNKS = BM * (BK / 8) / THREADS;   // 16-byte chunks per thread
-  static constexpr int B_THREADS = BN;                       // threads owning an 8 x 8 block
+  static constexpr int A_STAGE = BM * BK * 2;        // bytes
+  static constexpr int B_STAGE = BK * BN * 2;
+  static constexpr int A_DMA = A_STAGE / 1024 / 4;   // 1 KB loads per wave per slab
+  static constexpr int B_DMA = B_STAGE / 1024 / 4;
+  static constexpr int DMA = A_DMA + B_DMA;
+  static constexpr int B_ROW = BN * 2;               // bytes per LDS row of B
+  static constexpr int B_CPR = BN / 8;               // 16-byte chunks per B row
+  static constexpr int LDS_BYTES = STAGES * (A_STAGE + B_STAGE);
   static_assert(BM % 128 == 0 && BN % 128 == 0, "blocks are whole 128 x 128 tiles");
 };
 
-// Byte offset of 16-byte chunk kc (0..7) of LDS row `row` (128-byte rows).
-__device__ __forceinline__ int lds_off(int row, int kc) {
-  return row * 128 + (((kc ^ row ^ (row >> 3)) & 7) << 4);
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  // C-style cast: generic -> LDS address space (no C++ cast performs it).
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 64 lanes x 16 bytes from `src` (per lane) into LDS [lds, lds + 1 KB).  The
+// load is hidden from the compiler's wait tracking; callers wait with
+// wait_vm<N>() before a barrier that precedes any read of the data.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -75,22 +111,110 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, b);
 }
 
+__device__ __forceinline__ bf16x4_t ds_read_tr(const char* p) {
+  typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+  i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(__attribute__((address_space(3))) char*)p);
+  return __builtin_bit_cast(bf16x4_t, v);
+}
+
 template <int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   using S = GemmShape<BM, BN>;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  // One LDS arena: 4 A stages, then 4 B stages; reused for the C tile at the end.
+  __shared__ __attribute__((aligned(1024))) char smem[S::LDS_BYTES];
+  char* const sA[4] = {smem, smem + S::A_STAGE, smem + 2 * S::A_STAGE, smem + 3 * S::A_STAGE};
+  char* const sB[4] = {smem + 4 * S::A_STAGE, smem + 4 * S::A_STAGE + S::B_STAGE,
+                       smem + 4 * S::A_STAGE + 2 * S::B_STAGE, smem + 4 * S::A_STAGE + 3 * S::B_STAGE};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
-  const BlockGrid grid = make_grid(a.M, a.N, a.P, BM, BN);
+  const BlockGrid grid = make_grid(a.M, a.N, a.P, BM, BN, a.group_m);
   const BlockPos bp = block_of_position(a.order, blockIdx.x, grid);
   const int row0 = bp.mb * BM;
   const int col0 = bp.nb * BN;
   const int K = a.K;
   const int nk = (K + S::BK - 1) / S::BK;
+
+  // ---- per-lane DMA sources (element offsets) and their K coordinate
+  const uint16_t* Ablk = a.A + static_cast<int64_t>(row0) * a.lda;
+  const uint16_t* Bblk = a.B + col0;
+  int64_t a_off[S::A_DMA], b_off[S::B_DMA];
+  int a_k[S::A_DMA], b_k[S::B_DMA];
+#pragma unroll
+  for (int i = 0; i < S::A_DMA; ++i) {
+    const int r = (wave * S::A_DMA + i) * 16 + (lane >> 2);
+    const int lc = (lane & 3) ^ ((r >> 2) & 3);
+    a_off[i] = static_cast<int64_t>(r) * a.lda + lc * 8;
+    a_k[i] = lc * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < S::B_DMA; ++i) {
+    const int fc = (wave * S::B_DMA + i) * 64 + lane;
+    const int r = fc / S::B_CPR;
+    const int lc = (fc % S::B_CPR) ^ (4 * (r & 3));
+    b_off[i] = static_cast<int64_t>(r) * a.ldb + lc * 8;
+    b_k[i] = r;
+  }
+
+  auto dma_slab = [&](int kt, auto STG) {
+    constexpr int s = decltype(STG)::value;
+    const int k0 = kt * S::BK;
+#pragma unroll
+    for (int i = 0; i < S::A_DMA; ++i) {
+      const void* src = (k0 + a_k[i] < K) ? static_cast<const void*>(Ablk + a_off[i] + k0)
+                                          : static_cast<const void*>(a.zeros);
+      dma16(src, lds_u32(sA[s] + (wave * S::A_DMA + i) * 1024));
+    }
+#pragma unroll
+    for (int i = 0; i < S::B_DMA; ++i) {
+      const void* src = (k0 + b_k[i] < K)
+                            ? static_cast<const void*>(Bblk + b_off[i] + static_cast<int64_t>(k0) * a.ldb)
+                            : static_cast<const void*>(a.zeros);
+      dma16(src, lds_u32(sB[s] + (wave * S::B_DMA + i) * 1024));
+    }
+  };
+
+  // ---- per-lane LDS read offsets (bytes, relative to a stage)
+  // A fragment (rows wm*WM + i*32 + lane%32, 8 k per lane at 16 kk + 8 (lane/32)).
+  const int a_row = wm * S::WM + (lane & 31);
+  const int a_rd0 = a_row * 64 + (((lane >> 5) ^ ((a_row >> 2) & 3)) << 4);
+  const int a_rd1 = a_row * 64 + (((2 + (lane >> 5)) ^ ((a_row >> 2) & 3)) << 4);
+  // B fragment via transpose reads: lane = 16 g + i; reads row
+  // k = 16 kk + 8 (g / 2) + 4 h + i / 4, columns n .. n+3 with
+  // n = wn*WN + 32 j + 16 (g % 2) + 4 (i % 4).
+  const int b_kq = (lane >> 2) & 3;                       // k & 3 of the row read
+  const int b_row = (8 * (lane >> 5) + b_kq) * S::B_ROW;  // + (16 kk + 4 h) * B_ROW
+  int b_col[S::FN];
+#pragma unroll
+  for (int j = 0; j < S::FN; ++j) {
+    const int n = wn * S::WN + 32 * j + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    b_col[j] = (((n >> 3) ^ (4 * b_kq)) << 4) + ((n & 7) << 1);
+  }
+
+  struct Frags {
+    bf16x8_t a[2][S::FM];
+    bf16x8_t b[2][S::FN];
+  };
+  auto read_frags = [&](Frags& f, auto STG) {
+    constexpr int s = decltype(STG)::value;
+    const char* As = sA[s];
+    const char* Bs = sB[s];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int i = 0; i < S::FM; ++i)
+        f.a[kk][i] = *reinterpret_cast<const bf16x8_t*>(As + (kk ? a_rd1 : a_rd0) + i * 32 * 64);
+#pragma unroll
+      for (int j = 0; j < S::FN; ++j) {
+        const bf16x4_t lo = ds_read_tr(Bs + b_row + (16 * kk + 0) * S::B_ROW + b_col[j]);
+        const bf16x4_t hi = ds_read_tr(Bs + b_row + (16 * kk + 4) * S::B_ROW + b_col[j]);
+        f.b[kk][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
+  };
 
   f32x16_t acc[S::FM][S::FN];
 #pragma unroll
@@ -100,120 +224,101 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-  u32x4_t ra[S::A_CHUNKS];
-  u32x4_t rb[8];
-  const bool b_owner = tid < S::B_THREADS;
-  const int b_nc = tid % (BN / 8);   // 8-column group of the thread's 8 x 8 block
-  const int b_kg = tid / (BN / 8);   // 8-row (K) group
-
-  const uint16_t* Ablk = a.A + static_cast<int64_t>(row0) * a.lda;
-  const uint16_t* Bblk = a.B + col0 + b_nc * 8;
-
-  auto gload = [&](int kt) {
-    const int k0 = kt * S::BK;
+  auto mfma_half = [&](const Frags& f, auto KK) {
+    constexpr int kk = decltype(KK)::value;
 #pragma unroll
-    for (int i = 0; i < S::A_CHUNKS; ++i) {
-      const int ci = tid + S::THREADS * i;
-      const int r = ci >> 3, kc = ci & 7;
-      const int k = k0 + kc * 8;
-      ra[i] = (k < K) ? *reinterpret_cast<const u32x4_t*>(Ablk + static_cast<int64_t>(r) * a.lda + k)
-                      : u32x4_t{0, 0, 0, 0};
-    }
-    if (b_owner) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int k = k0 + b_kg * 8 + j;
-        rb[j] = (k < K) ? *reinterpret_cast<const u32x4_t*>(Bblk + static_cast<int64_t>(k) * a.ldb)
-                        : u32x4_t{0, 0, 0, 0};
-      }
-    }
-  };
-
-  auto lstore = [&](int stage) {
-    char* As = smem + stage * S::STAGE;
-    char* Bs = As + S::A_BYTES;
-#pragma unroll
-    for (int i = 0; i < S::A_CHUNKS; ++i) {
-      const int ci = tid + S::THREADS * i;
-      *reinterpret_cast<u32x4_t*>(As + lds_off(ci >> 3, ci & 7)) = ra[i];
-    }
-    if (b_owner) {
-      // rb[j] holds B[k = 8 kg + j][n = 8 nc .. 8 nc + 7]; column i of that
-      // 8 x 8 block becomes row n = 8 nc + i of the transposed slab.
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        u32x4_t t;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t x = rb[2 * q][i >> 1];
-          const uint32_t y = rb[2 * q + 1][i >> 1];
-          t[q] = (i & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
-        }
-        *reinterpret_cast<u32x4_t*>(Bs + lds_off(b_nc * 8 + i, b_kg)) = t;
-      }
-    }
-  };
-
-  auto compute = [&](int stage) {
-    const char* As = smem + stage * S::STAGE;
-    const char* Bs = As + S::A_BYTES;
-#pragma unroll
-    for (int kk = 0; kk < S::BK / 16; ++kk) {
-      const int kc = kk * 2 + (lane >> 5);
-      bf16x8_t af[S::FM], bfr[S::FN];
-#pragma unroll
-      for (int i = 0; i < S::FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(As + lds_off(wm * S::WM + i * 32 + (lane & 31), kc));
+    for (int i = 0; i < S::FM; ++i)
 #pragma unroll
       for (int j = 0; j < S::FN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + lds_off(wn * S::WN + j * 32 + (lane & 31), kc));
-#pragma unroll
-      for (int i = 0; i < S::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < S::FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
-    }
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[kk][j], f.a[kk][i], acc[i][j], 0, 0, 0);
   };
 
-  gload(0);
-  lstore(0);
+  Frags F0, F1;
+
+  // ---- prologue: slabs 0..2 in flight, slab 0 visible, its fragments read
+  dma_slab(0, IC<0>{});
+  if (nk > 1) dma_slab(1, IC<1>{});
+  if (nk > 2) dma_slab(2, IC<2>{});
+  if (nk > 2) wait_vm<2 * S::DMA>();
+  else if (nk > 1) wait_vm<S::DMA>();
+  else wait_vm<0>();
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(cur);
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
+  read_frags(F0, IC<0>{});
+
+  // ---- main loop, unrolled by the stage count so every stage index is static.
+  // The wait + barrier are unconditional so that the fragments of the
+  // current slab are complete on every path and the MFMAs never wait for the
+  // next slab's reads.
+  auto iter = [&](int kt, auto STG) {
+    constexpr int s = decltype(STG)::value;
+    Frags& cur = (s & 1) ? F1 : F0;
+    Frags& nxt = (s & 1) ? F0 : F1;
+    if (kt + 2 < nk) wait_vm<S::DMA>();   // slab kt+2 may stay in flight
+    else wait_vm<0>();
+    __syncthreads();                      // slab kt+1 landed for every wave;
+                                          // the stage of slab kt-1 is free
+    if (kt + 1 < nk) read_frags(nxt, IC<(s + 1) % 4>{});
+    mfma_half(cur, IC<0>{});
+    if (kt + 3 < nk) dma_slab(kt + 3, IC<(s + 3) % 4>{});
+    mfma_half(cur, IC<1>{});
+  };
+  for (int kt = 0; kt < nk; kt += 4) {
+    iter(kt, IC<0>{});
+    if (kt + 1 < nk) iter(kt + 1, IC<1>{});
+    if (kt + 2 < nk) iter(kt + 2, IC<2>{});
+    if (kt + 3 < nk) iter(kt + 3, IC<3>{});
   }
 
-  // Epilogue: lane holds D[n][m] for m = lane % 32 and
-  // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T).
+  // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
+  // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T), i.e. 4
+  // consecutive columns of one row per group of 4 registers.  Each wave
+  // stages its (BM/2) x (BN/2) sub-block in its own LDS region (rows of
+  // BN/2 bf16, 16-byte chunks XOR-swizzled by row), then stores whole rows
+  // with 16-byte lanes: every store instruction writes full 128-byte lines.
+  // The stores are non-temporal: the partial is read once, by the reducer,
+  // and streaming it past L2 leaves little dirty data for the release fence
+  // to write back.
+  constexpr int CPR = S::WN / 8;                 // 16-byte chunks per staged row
+  constexpr int ROWB = S::WN * 2;                // bytes per staged row
+  char* const cst = smem + wave * (S::WM * ROWB);
+  static_assert(4 * S::WM * ROWB <= S::LDS_BYTES, "C tile fits the LDS arena");
+  __syncthreads();                               // all waves are done with the stages
 #pragma unroll
   for (int i = 0; i < S::FM; ++i) {
-    const int m = row0 + wm * S::WM + i * 32 + (lane & 31);
-    uint16_t* crow = a.C + static_cast<int64_t>(m) * a.ldc;
+    const int r = i * 32 + (lane & 31);
 #pragma unroll
-    for (int j = 0; j < S::FN; ++j) {
+    for (int j = 0; j < S::FN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = col0 + wn * S::WN + j * 32 + g * 8 + (lane >> 5) * 4;
+        const int c = 4 * j + g;                 // chunk of columns 32 j + 8 g .. + 7
         u32x2_t w;
         w[0] = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
         w[1] = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-        *reinterpret_cast<u32x2_t*>(crow + n) = w;
+        *reinterpret_cast<u32x2_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4) + (lane >> 5) * 8) = w;
       }
-    }
+  }
+  // Rows are private to the wave: only the wave's own LDS writes must land.
+  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  constexpr int RPI = 64 / CPR;                  // rows per store instruction
+  uint16_t* cblk = a.C + static_cast<int64_t>(row0 + wm * S::WM) * a.ldc + col0 + wn * S::WN;
+#pragma unroll
+  for (int r0 = 0; r0 < S::WM; r0 += RPI) {
+    const int r = r0 + lane / CPR, c = lane % CPR;
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4));
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(cblk + static_cast<int64_t>(r) * a.ldc + c * 8));
   }
 
   if (a.flags != nullptr) {
     __syncthreads();
     if (tid == 0) {
       const int tiles_n = a.N / kTile;
+      release_fence();
 #pragma unroll
       for (int ti = 0; ti < BM / kTile; ++ti)
 #pragma unroll
         for (int tj = 0; tj < BN / kTile; ++tj)
-          publish_release(a.flags + (bp.mb * (BM / kTile) + ti) * tiles_n + bp.nb * (BN / kTile) + tj,
+          publish_relaxed(a.flags + (bp.mb * (BM / kTile) + ti) * tiles_n + bp.nb * (BN / kTile) + tj,
                           a.epoch);
     }
   }

@@ -32,7 +32,7 @@ struct ReduceArgs {
   const uint16_t* peers[ENTWINE_MAX_P - 1];
   uint16_t* out;
   int64_t ldc, ldp, ldo;
-  int M, N, dest, x, BM, BN;
+  int M, N, dest, x, BM, BN, group_m;
   const int* flags;        // local flags, one per global tile
   const int* peer_flags;   // (P-1) x ntiles synthetic peer flags
   uint32_t epoch;
@@ -61,7 +61,7 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
   static_assert(VPT % G == 0, "batch must divide the per-thread vectors");
   __shared__ int s_abort;
 
-  const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN);
+  const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
   const int Q = tiles_per_partition(a.M, a.N, NP);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;

@@ -37,7 +37,7 @@ class Config(ctypes.Structure):
     _fields_ = [("order", ctypes.c_int32), ("gemm_cfg", ctypes.c_int32),
                 ("reduce_wgs", ctypes.c_int32), ("reduce_threads", ctypes.c_int32),
                 ("timeout_us", ctypes.c_int32), ("withhold_peer", ctypes.c_int32),
-                ("record_timing", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("record_timing", ctypes.c_int32), ("group_m", ctypes.c_int32)]
 
     @classmethod
     def make(cls, **kw) -> "Config":
@@ -64,7 +64,7 @@ _PROTOS = {
     "entwine_last_timing": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
     "entwine_validate": (_i32, [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(Config)]),
-    "entwine_tile_schedule": (_i32, [_i32, _i64, _i64, _i32, _i32, _i32, _P32, _P32]),
+    "entwine_tile_schedule": (_i32, [_i32, _i64, _i64, _i32, _i32, _i32, _i32, _P32, _P32]),
     "entwine_consumer_tasks": (_i32, [_i32, _i32, _i32, _i32, _i32, _P32, _P32, _i32, _P32]),
     "entwine_status_string": (ctypes.c_char_p, [_i32]),
     "entwine_last_error": (ctypes.c_char_p, [_vp]),
@@ -110,13 +110,13 @@ def validate(M, N, K, P, dest, cfg: Config | None = None) -> int:
     return lib().entwine_validate(M, N, K, P, dest, ctypes.byref(cfg) if cfg else None)
 
 
-def tile_schedule(order: int, M: int, N: int, P: int, BM: int, BN: int):
+def tile_schedule(order: int, M: int, N: int, P: int, BM: int, BN: int, group_m: int = 1):
     """Traversal as computed by the library: (blocks[p] = (d, l, mb, nb),
     tiles[tile_row, tile_col] = (d, t))."""
     nb = (M // BM) * (N // BN)
     blocks = np.zeros((nb, 4), np.int32)
     tiles = np.zeros((M // TILE, N // TILE, 2), np.int32)
-    _check(lib().entwine_tile_schedule(order, M, N, P, BM, BN, blocks.ctypes.data_as(_P32),
+    _check(lib().entwine_tile_schedule(order, M, N, P, BM, BN, group_m, blocks.ctypes.data_as(_P32),
                                        tiles.ctypes.data_as(_P32)))
     return blocks, tiles
 

@@ -80,9 +80,10 @@ SHAPES = [(512, 1024, 2, 256, 256), (4096, 4096, 8, 256, 256), (4096, 4096, 8, 1
 
 @pytest.mark.parametrize("M,N,P,BM,BN", SHAPES)
 @pytest.mark.parametrize("order", [S.INTERLEAVED, S.ROW_MAJOR, S.M_MAJOR])
-def test_library_schedule_matches_oracle(lib, M, N, P, BM, BN, order):
-    blocks, tiles = E.tile_schedule(order, M, N, P, BM, BN)
-    ref = S.full_schedule(order, M, N, P, BM, BN)
+@pytest.mark.parametrize("group_m", [1, 2, 4, 8])
+def test_library_schedule_matches_oracle(lib, M, N, P, BM, BN, order, group_m):
+    blocks, tiles = E.tile_schedule(order, M, N, P, BM, BN, group_m)
+    ref = S.full_schedule(order, M, N, P, BM, BN, group_m)
     assert blocks.tolist() == [[d, l, mb, nb] for d, l, mb, nb, _ in ref]
     want = np.full(tiles.shape, -1, np.int32)
     for d, _, _, _, tl in ref:
@@ -104,6 +105,8 @@ def test_library_consumer_tasks_match_oracle(lib, P, Q, x):
 def test_schedule_rejects_bad_blocks(lib):
     with pytest.raises(E.EntwineError):
         E.tile_schedule(0, 512, 1024, 2, 512, 256)
+    with pytest.raises(E.EntwineError):
+        E.tile_schedule(0, 512, 1024, 2, 256, 256, 65)
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -129,6 +129,7 @@ def test_results_independent_of_order_budget_threads_and_mode():
         torch.cuda.synchronize()
         check_rows(prob, base[::37], np.arange(M)[::37])
         variants = [dict(order=o) for o in (1, 2)] + [dict(gemm_cfg=c) for c in (1, 2, 3)] + \
+                   [dict(group_m=g) for g in (1, 2, 8)] + [dict(order=2, group_m=1)] + \
                    [dict(reduce_wgs=x) for x in (4, 8, 32, 64)] + \
                    [dict(reduce_threads=b) for b in (128, 512)]
         for kw in variants:

@@ -58,8 +58,9 @@ SHAPES = [(512, 1024, 2, 256, 256), (4096, 4096, 8, 256, 256), (1024, 768, 4, 12
 
 @pytest.mark.parametrize("M,N,P,BM,BN", SHAPES)
 @pytest.mark.parametrize("order", [S.INTERLEAVED, S.ROW_MAJOR, S.M_MAJOR])
-def test_schedule_is_a_bijection_onto_blocks_and_tiles(M, N, P, BM, BN, order):
-    sched = S.full_schedule(order, M, N, P, BM, BN)
+@pytest.mark.parametrize("group_m", [1, 4])
+def test_schedule_is_a_bijection_onto_blocks_and_tiles(M, N, P, BM, BN, order, group_m):
+    sched = S.full_schedule(order, M, N, P, BM, BN, group_m)
     nb = (M // BM) * (N // BN)
     assert len({(s[2], s[3]) for s in sched}) == nb
     Q = S.tiles_per_partition(M, N, P)
@@ -75,12 +76,13 @@ def test_schedule_is_a_bijection_onto_blocks_and_tiles(M, N, P, BM, BN, order):
 
 
 @pytest.mark.parametrize("M,N,P,BM,BN", SHAPES)
-def test_interleaved_local_blocks_are_p_apart(M, N, P, BM, BN):
-    sched = S.full_schedule(S.INTERLEAVED, M, N, P, BM, BN)
+@pytest.mark.parametrize("group_m", [1, 4])
+def test_interleaved_local_blocks_are_p_apart(M, N, P, BM, BN, group_m):
+    sched = S.full_schedule(S.INTERLEAVED, M, N, P, BM, BN, group_m)
     for r in range(P):
         pos = [p for p, s in enumerate(sched) if s[0] == r]
         assert pos[0] == r and all(b - a == P for a, b in zip(pos, pos[1:]))
-        # within a partition, production follows the consumer's N-major order
+        # within a partition, production follows the partition walk (the consumer's order)
         assert [sched[p][1] for p in pos] == list(range(len(pos)))
 
 
@@ -116,3 +118,24 @@ def test_all_chunk_assignment_splits_budget_evenly():
     assert all(sorted(v) == list(range(Q)) for v in cover.values())
     with pytest.raises(ValueError):
         S.all_chunk_consumer_tasks(0, 6, 4, Q)
+
+
+def test_grouped_walk_keeps_xcd_patches_compact():
+    """With P = 8 every partition runs on one XCD; 32 consecutive blocks of
+    the grouped walk (group_m = 4) touch 4 block rows and 8 block columns,
+    against 1 row and 32 columns for the N-major walk."""
+    RB, NB = 4, 32
+    for gm, rows, cols in ((4, 4, 8), (1, 1, 32)):
+        walk = S.partition_walk(RB, NB, 8, gm)
+        assert sorted(walk) == [(r, c) for r in range(RB) for c in range(NB)]
+        first = walk[:32]
+        assert len({r for r, _ in first}) == rows and len({c for _, c in first}) == cols
+
+
+def test_grouped_walk_stripes_follow_xcds():
+    """P = 2: blocks of partition d at positions p = 2 l + d run on XCD
+    p mod 8, i.e. stripe l mod 4; each stripe is a fixed quarter of the columns."""
+    RB, NB, P = 4, 16, 2
+    walk = S.partition_walk(RB, NB, P, 4)
+    for l, (r, c) in enumerate(walk):
+        assert c // 4 == l % 4
