@@ -38,6 +38,7 @@ def parse():
     ap.add_argument("--x", type=int, default=None, help="reducer workgroups (communication budget)")
     ap.add_argument("--b", type=int, default=None, help="reducer threads per workgroup")
     ap.add_argument("--group-m", type=int, default=None, help="block walk inside a partition (1 = N-major)")
+    ap.add_argument("--gemm-wgs", type=int, default=None, help="producer workgroups (persistent grid)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-legs", action="store_true", help="skip the gemm-only / reduce-only / sequential legs")
     ap.add_argument("--only", default=None, choices=["fused", "gemm", "reduce", "seq"],
@@ -82,7 +83,7 @@ def main():
     tuned = tuned_config(w.name, "all" if all_chunks else "rank")
     kw = dict(tuned)
     for k, v in (("order", args.order), ("gemm_cfg", args.gemm_cfg), ("reduce_wgs", args.x),
-                 ("reduce_threads", args.b), ("group_m", args.group_m)):
+                 ("reduce_threads", args.b), ("group_m", args.group_m), ("gemm_wgs", args.gemm_wgs)):
         if v is not None:
             kw[k] = v
     cfg = E.Config.make(**kw, record_timing=1)
@@ -196,7 +197,7 @@ def main():
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "P": P,
                    "dest": "all" if all_chunks else dest_mode, "mode": main_mode,
                    "order": cfg.order, "gemm_cfg": cfg.gemm_cfg, "reduce_wgs": cfg.reduce_wgs,
-                   "reduce_threads": cfg.reduce_threads, "group_m": cfg.group_m},
+                   "reduce_threads": cfg.reduce_threads, "group_m": cfg.group_m, "gemm_wgs": cfg.gemm_wgs},
         "roofline": {"bound": "mfma", "kernel": "gemm_producer",
                      "achieved": round(achieved, 2) if achieved else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

@@ -88,6 +88,11 @@ typedef struct {
   int32_t group_m;        /* block order inside a partition: 1 = N-major (the
                              paper's), g > 1 = XCD-striped walk in groups of g
                              block rows (L2 reuse); 0 = default (4) */
+  int32_t gemm_wgs;       /* producer workgroups (persistent; each takes
+                             positions w, w + G, ...): 0 = default = the CUs,
+                             minus x in the fused path, rounded down to a
+                             multiple of 8 (one workgroup per CU) */
+  int32_t reserved;
 } entwine_config;
 
 /* Fill *cfg with the defaults. */

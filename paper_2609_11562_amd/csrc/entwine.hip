@@ -101,7 +101,7 @@ int default_gemm_cfg(int64_t M, int64_t N, int P) {
 }
 
 struct Resolved {
-  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m;
+  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m, gemm_wgs;
   uint64_t timeout_us;
 };
 
@@ -120,6 +120,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.timeout_us < 0) return fail(ctx, ENTWINE_EINVAL, "timeout_us must be >= 0");
   if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
   if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
+  if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -143,6 +144,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->timing = c.record_timing;
   r->timeout_us = c.timeout_us ? uint64_t(c.timeout_us) : 2000000ull;
   r->group_m = c.group_m ? c.group_m : 4;
+  r->gemm_wgs = c.gemm_wgs;
   return ENTWINE_OK;
 }
 
@@ -214,9 +216,24 @@ TimingSlot* timing_slot(entwine_ctx* ctx, const Resolved& r) {
   return s;
 }
 
+// Producer grid: persistent workgroups, one per CU, each walking positions
+// w, w + G, ...  G is a multiple of 8 so that position p keeps running on XCD
+// p mod 8 (workgroups are dispatched round-robin over the 8 XCDs).  In the
+// fused path the reducer's x workgroups get the remaining CUs.
+int producer_grid(const entwine_ctx* ctx, const Resolved& r, bool fused) {
+  const int nblk = int((ctx->M / r.BM) * (ctx->N / r.BN));
+  int g = r.gemm_wgs;
+  if (g <= 0) {
+    const int cus = ctx->cus > 0 ? ctx->cus : 256;
+    g = fused ? cus - r.x : cus;
+    g = std::max(8, (g / 8) * 8);
+  }
+  return std::min(g, nblk);
+}
+
 entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t lda, const void* B,
                            int64_t ldb, void* C, int64_t ldc, bool publish, uint32_t epoch,
-                           hipStream_t s) {
+                           hipStream_t s, bool fused) {
   GemmArgs g;
   g.A = static_cast<const uint16_t*>(A);
   g.B = static_cast<const uint16_t*>(B);
@@ -233,8 +250,7 @@ entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, i
   g.group_m = r.group_m;
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
-  const int nblocks = int((ctx->M / r.BM) * (ctx->N / r.BN));
-  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(nblocks), dim3(256), 0, s, g);
+  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(producer_grid(ctx, r, fused)), dim3(256), 0, s, g);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }
@@ -276,6 +292,13 @@ entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* pa
   return ENTWINE_OK;
 }
 
+// The producer addresses A and B with 32-bit byte offsets inside a block.
+entwine_status check_operand_ld(entwine_ctx* ctx, int64_t lda, int64_t ldb) {
+  if (lda > (int64_t(1) << 22) || ldb > (int64_t(1) << 22))
+    return fail(ctx, ENTWINE_EINVAL, "lda/ldb above 2^22 elements are not supported");
+  return ENTWINE_OK;
+}
+
 entwine_status check_peers(entwine_ctx* ctx, const void* const* peers, int64_t ldp) {
   if (ctx->P == 1) return ENTWINE_OK;
   if (!peers) return fail(ctx, ENTWINE_EINVAL, "peers is NULL with P > 1");
@@ -297,6 +320,8 @@ void entwine_config_default(entwine_config* cfg) {
   cfg->withhold_peer = -1;
   cfg->record_timing = 0;
   cfg->group_m = 0;
+  cfg->gemm_wgs = 0;
+  cfg->reserved = 0;
 }
 
 int32_t entwine_abi_version(void) { return ENTWINE_ABI_VERSION; }
@@ -398,6 +423,7 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
   CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, dest, cfg, ctx->cus, &r));
   CHECK(check_matrix(ctx, A, lda, ctx->K, "A"));
   CHECK(check_matrix(ctx, B, ldb, ctx->N, "B"));
+  CHECK(check_operand_ld(ctx, lda, ldb));
   CHECK(check_matrix(ctx, out, ldo, ctx->N, "out"));
   CHECK(check_peers(ctx, peers, ldp));
   if (partial) {
@@ -416,7 +442,7 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
 
   if (fused) HIP_OR_FAIL(ctx, hipEventRecord(ctx->ev_fork, gs));
   if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, gs));
-  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, gs));
+  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, gs, fused));
   if (ts) {
     HIP_OR_FAIL(ctx, hipEventRecord(ts->gemm_end, gs));
     ts->has_gemm = true;
@@ -443,6 +469,7 @@ entwine_status entwine_gemm_only(entwine_ctx* ctx, const void* A, int64_t lda, c
   CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, 0, cfg, ctx->cus, &r));
   CHECK(check_matrix(ctx, A, lda, ctx->K, "A"));
   CHECK(check_matrix(ctx, B, ldb, ctx->N, "B"));
+  CHECK(check_operand_ld(ctx, lda, ldb));
   if (partial) {
     CHECK(check_matrix(ctx, partial, ldc, ctx->N, "partial"));
   } else {
@@ -455,7 +482,7 @@ entwine_status entwine_gemm_only(entwine_ctx* ctx, const void* A, int64_t lda, c
   const uint32_t epoch = next_epoch(ctx);
   TimingSlot* ts = timing_slot(ctx, r);
   if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, s));
-  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, s));
+  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, s, false));
   if (ts) {
     HIP_OR_FAIL(ctx, hipEventRecord(ts->gemm_end, s));
     ts->has_gemm = true;

@@ -80,7 +80,8 @@ struct GemmShape {
   static constexpr int DMA = A_DMA + B_DMA;
   static constexpr int B_ROW = BN * 2;               // bytes per LDS row of B
   static constexpr int B_CPR = BN / 8;               // 16-byte chunks per B row
-  static constexpr int LDS_BYTES = STAGES * (A_STAGE + B_STAGE);
+  static constexpr int C_BYTES = 32 * 1024;           // epilogue staging, 8 KB per wave
+  static constexpr int LDS_BYTES = STAGES * (A_STAGE + B_STAGE) + C_BYTES;
   static_assert(BM % 128 == 0 && BN % 128 == 0, "blocks are whole 128 x 128 tiles");
 };
 
@@ -95,8 +96,28 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 // 64 lanes x 16 bytes from `src` (per lane) into LDS [lds, lds + 1 KB).  The
 // load is hidden from the compiler's wait tracking; callers wait with
 // wait_vm<N>() before a barrier that precedes any read of the data.
+// The compiler does not insert hazard wait states for operands of inline
+// asm, so the asm carries them: GFX9 needs 1 wait state between a scalar
+// write of M0 and an LDS-DMA load reading it.
 __device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+// Same, addressing with a wave-uniform 64-bit base and a 32-bit per-lane
+// byte offset (the saddr form): no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// The base usually arrives through v_readfirstlane (a VALU write of an
+// SGPR); GFX9 needs 5 wait states between that and a VMEM instruction
+// reading the SGPR, which also covers the M0 wait state above.
+__device__ __forceinline__ void dma16_s(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(uniform_ptr(base)), "{m0}"(lds)
+               : "memory");
 }
 
 template <int N>
@@ -120,34 +141,38 @@ __device__ __forceinline__ bf16x4_t ds_read_tr(const char* p) {
 template <int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   using S = GemmShape<BM, BN>;
-  // One LDS arena: 4 A stages, then 4 B stages; reused for the C tile at the end.
+  // LDS: 4 A stages, 4 B stages, then a C staging area (8 KB per wave).
   __shared__ __attribute__((aligned(1024))) char smem[S::LDS_BYTES];
-  char* const sA[4] = {smem, smem + S::A_STAGE, smem + 2 * S::A_STAGE, smem + 3 * S::A_STAGE};
-  char* const sB[4] = {smem + 4 * S::A_STAGE, smem + 4 * S::A_STAGE + S::B_STAGE,
-                       smem + 4 * S::A_STAGE + 2 * S::B_STAGE, smem + 4 * S::A_STAGE + 3 * S::B_STAGE};
+  char* const sA = smem;
+  char* const sB = smem + 4 * S::A_STAGE;
+  char* const sC = smem + 4 * (S::A_STAGE + S::B_STAGE);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
+  // ---- work of this workgroup: logical positions p = w, w + G, w + 2G, ...
+  // Positions are taken in increasing order, so production time follows the
+  // logical order of the traversal; all its K-slabs form one stream, so the
+  // loads of the next block start while the current block finishes.
   const BlockGrid grid = make_grid(a.M, a.N, a.P, BM, BN, a.group_m);
-  const BlockPos bp = block_of_position(a.order, blockIdx.x, grid);
-  const int row0 = bp.mb * BM;
-  const int col0 = bp.nb * BN;
+  const int nblk = grid.MB * grid.NB;
+  const int G = gridDim.x, w = blockIdx.x;
+  const int mine = w < nblk ? (nblk - 1 - w) / G + 1 : 0;
   const int K = a.K;
   const int nk = (K + S::BK - 1) / S::BK;
+  const int total = mine * nk;
+  if (total == 0) return;
 
-  // ---- per-lane DMA sources (element offsets) and their K coordinate
-  const uint16_t* Ablk = a.A + static_cast<int64_t>(row0) * a.lda;
-  const uint16_t* Bblk = a.B + col0;
-  int64_t a_off[S::A_DMA], b_off[S::B_DMA];
+  // ---- per-lane DMA sources: byte offsets inside a block, and their K
+  uint32_t a_off[S::A_DMA], b_off[S::B_DMA];
   int a_k[S::A_DMA], b_k[S::B_DMA];
 #pragma unroll
   for (int i = 0; i < S::A_DMA; ++i) {
     const int r = (wave * S::A_DMA + i) * 16 + (lane >> 2);
     const int lc = (lane & 3) ^ ((r >> 2) & 3);
-    a_off[i] = static_cast<int64_t>(r) * a.lda + lc * 8;
+    a_off[i] = static_cast<uint32_t>((r * a.lda + lc * 8) * 2);
     a_k[i] = lc * 8;
   }
 #pragma unroll
@@ -155,25 +180,39 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
     const int fc = (wave * S::B_DMA + i) * 64 + lane;
     const int r = fc / S::B_CPR;
     const int lc = (fc % S::B_CPR) ^ (4 * (r & 3));
-    b_off[i] = static_cast<int64_t>(r) * a.ldb + lc * 8;
+    b_off[i] = static_cast<uint32_t>((r * a.ldb + lc * 8) * 2);
     b_k[i] = r;
   }
 
-  auto dma_slab = [&](int kt, auto STG) {
-    constexpr int s = decltype(STG)::value;
-    const int k0 = kt * S::BK;
+  // DMA cursor: the next slab of the stream to load (block d_lb, slab d_kt).
+  int d_g = 0, d_kt = 0, d_lb = 0;
+  BlockPos d_bp = block_of_position(a.order, w, grid);
+  auto dma_next = [&]() {
+    const int st = d_g & 3;
+    const int k0 = d_kt * S::BK;
+    const char* Ab = reinterpret_cast<const char*>(a.A + static_cast<int64_t>(d_bp.mb * BM) * a.lda + k0);
+    const char* Bb = reinterpret_cast<const char*>(a.B + static_cast<int64_t>(k0) * a.ldb + d_bp.nb * BN);
+    const uint32_t la = lds_u32(sA + st * S::A_STAGE + wave * S::A_DMA * 1024);
+    const uint32_t lb = lds_u32(sB + st * S::B_STAGE + wave * S::B_DMA * 1024);
+    if (k0 + S::BK <= K) {                      // whole slab inside K
 #pragma unroll
-    for (int i = 0; i < S::A_DMA; ++i) {
-      const void* src = (k0 + a_k[i] < K) ? static_cast<const void*>(Ablk + a_off[i] + k0)
-                                          : static_cast<const void*>(a.zeros);
-      dma16(src, lds_u32(sA[s] + (wave * S::A_DMA + i) * 1024));
+      for (int i = 0; i < S::A_DMA; ++i) dma16_s(Ab, a_off[i], la + i * 1024);
+#pragma unroll
+      for (int i = 0; i < S::B_DMA; ++i) dma16_s(Bb, b_off[i], lb + i * 1024);
+    } else {                                    // K tail: lanes past K read zeros
+#pragma unroll
+      for (int i = 0; i < S::A_DMA; ++i)
+        dma16((k0 + a_k[i] < K) ? static_cast<const void*>(Ab + a_off[i]) : static_cast<const void*>(a.zeros),
+              la + i * 1024);
+#pragma unroll
+      for (int i = 0; i < S::B_DMA; ++i)
+        dma16((k0 + b_k[i] < K) ? static_cast<const void*>(Bb + b_off[i]) : static_cast<const void*>(a.zeros),
+              lb + i * 1024);
     }
-#pragma unroll
-    for (int i = 0; i < S::B_DMA; ++i) {
-      const void* src = (k0 + b_k[i] < K)
-                            ? static_cast<const void*>(Bblk + b_off[i] + static_cast<int64_t>(k0) * a.ldb)
-                            : static_cast<const void*>(a.zeros);
-      dma16(src, lds_u32(sB[s] + (wave * S::B_DMA + i) * 1024));
+    ++d_g;
+    if (++d_kt == nk) {
+      d_kt = 0;
+      if (++d_lb < mine) d_bp = block_of_position(a.order, w + d_lb * G, grid);
     }
   };
 
@@ -194,132 +233,124 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
     b_col[j] = (((n >> 3) ^ (4 * b_kq)) << 4) + ((n & 7) << 1);
   }
 
+  // Fragments of one K-half (16 k) of a slab.
   struct Frags {
-    bf16x8_t a[2][S::FM];
-    bf16x8_t b[2][S::FN];
+    bf16x8_t a[S::FM];
+    bf16x8_t b[S::FN];
   };
-  auto read_frags = [&](Frags& f, auto STG) {
-    constexpr int s = decltype(STG)::value;
-    const char* As = sA[s];
-    const char* Bs = sB[s];
+  auto read_half = [&](Frags& f, int st, auto KK) {
+    constexpr int kk = decltype(KK)::value;
+    const char* As = sA + st * S::A_STAGE + (kk ? a_rd1 : a_rd0);
+    const char* Bs = sB + st * S::B_STAGE + b_row + 16 * kk * S::B_ROW;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int i = 0; i < S::FM; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(As + i * 32 * 64);
 #pragma unroll
-      for (int i = 0; i < S::FM; ++i)
-        f.a[kk][i] = *reinterpret_cast<const bf16x8_t*>(As + (kk ? a_rd1 : a_rd0) + i * 32 * 64);
-#pragma unroll
-      for (int j = 0; j < S::FN; ++j) {
-        const bf16x4_t lo = ds_read_tr(Bs + b_row + (16 * kk + 0) * S::B_ROW + b_col[j]);
-        const bf16x4_t hi = ds_read_tr(Bs + b_row + (16 * kk + 4) * S::B_ROW + b_col[j]);
-        f.b[kk][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
+    for (int j = 0; j < S::FN; ++j) {
+      const bf16x4_t lo = ds_read_tr(Bs + b_col[j]);
+      const bf16x4_t hi = ds_read_tr(Bs + 4 * S::B_ROW + b_col[j]);
+      f.b[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
   };
 
   f32x16_t acc[S::FM][S::FN];
-#pragma unroll
-  for (int i = 0; i < S::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < S::FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-
-  auto mfma_half = [&](const Frags& f, auto KK) {
-    constexpr int kk = decltype(KK)::value;
+  auto mfma_half = [&](const Frags& f) {
 #pragma unroll
     for (int i = 0; i < S::FM; ++i)
 #pragma unroll
       for (int j = 0; j < S::FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[kk][j], f.a[kk][i], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
   };
 
-  Frags F0, F1;
+  // One slab g of the stream.  On entry X holds the first K-half of slab g.
+  // Read the second half into Y and multiply X; then make slab g+1 visible
+  // (own loads done, barrier - which also frees the stage of slab g-1), read
+  // its first half into X, queue the loads of slab g+3 into the freed stage,
+  // and multiply Y.  The wait and barrier are unconditional so that every
+  // path reaches the MFMAs with its operands complete.
+  Frags X, Y;
+  auto step = [&](int g) {
+    read_half(Y, g & 3, IC<1>{});
+    mfma_half(X);
+    if (g + 2 < total) wait_vm<S::DMA>();
+    else wait_vm<0>();
+    __syncthreads();
+    if (g + 1 < total) read_half(X, (g + 1) & 3, IC<0>{});
+    if (g + 3 < total) dma_next();
+    mfma_half(Y);
+  };
 
-  // ---- prologue: slabs 0..2 in flight, slab 0 visible, its fragments read
-  dma_slab(0, IC<0>{});
-  if (nk > 1) dma_slab(1, IC<1>{});
-  if (nk > 2) dma_slab(2, IC<2>{});
-  if (nk > 2) wait_vm<2 * S::DMA>();
-  else if (nk > 1) wait_vm<S::DMA>();
+  dma_next();
+  if (total > 1) dma_next();
+  if (total > 2) dma_next();
+  if (total > 2) wait_vm<2 * S::DMA>();
+  else if (total > 1) wait_vm<S::DMA>();
   else wait_vm<0>();
   __syncthreads();
-  read_frags(F0, IC<0>{});
+  read_half(X, 0, IC<0>{});
 
-  // ---- main loop, unrolled by the stage count so every stage index is static.
-  // The wait + barrier are unconditional so that the fragments of the
-  // current slab are complete on every path and the MFMAs never wait for the
-  // next slab's reads.
-  auto iter = [&](int kt, auto STG) {
-    constexpr int s = decltype(STG)::value;
-    Frags& cur = (s & 1) ? F1 : F0;
-    Frags& nxt = (s & 1) ? F0 : F1;
-    if (kt + 2 < nk) wait_vm<S::DMA>();   // slab kt+2 may stay in flight
-    else wait_vm<0>();
-    __syncthreads();                      // slab kt+1 landed for every wave;
-                                          // the stage of slab kt-1 is free
-    if (kt + 1 < nk) read_frags(nxt, IC<(s + 1) % 4>{});
-    mfma_half(cur, IC<0>{});
-    if (kt + 3 < nk) dma_slab(kt + 3, IC<(s + 3) % 4>{});
-    mfma_half(cur, IC<1>{});
-  };
-  for (int kt = 0; kt < nk; kt += 4) {
-    iter(kt, IC<0>{});
-    if (kt + 1 < nk) iter(kt + 1, IC<1>{});
-    if (kt + 2 < nk) iter(kt + 2, IC<2>{});
-    if (kt + 3 < nk) iter(kt + 3, IC<3>{});
-  }
-
-  // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
-  // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T), i.e. 4
-  // consecutive columns of one row per group of 4 registers.  Each wave
-  // stages its (BM/2) x (BN/2) sub-block in its own LDS region (rows of
-  // BN/2 bf16, 16-byte chunks XOR-swizzled by row), then stores whole rows
-  // with 16-byte lanes: every store instruction writes full 128-byte lines.
-  // The stores are non-temporal: the partial is read once, by the reducer,
-  // and streaming it past L2 leaves little dirty data for the release fence
-  // to write back.
   constexpr int CPR = S::WN / 8;                 // 16-byte chunks per staged row
   constexpr int ROWB = S::WN * 2;                // bytes per staged row
-  char* const cst = smem + wave * (S::WM * ROWB);
-  static_assert(4 * S::WM * ROWB <= S::LDS_BYTES, "C tile fits the LDS arena");
-  __syncthreads();                               // all waves are done with the stages
-#pragma unroll
-  for (int i = 0; i < S::FM; ++i) {
-    const int r = i * 32 + (lane & 31);
-#pragma unroll
-    for (int j = 0; j < S::FN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = 4 * j + g;                 // chunk of columns 32 j + 8 g .. + 7
-        u32x2_t w;
-        w[0] = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
-        w[1] = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-        *reinterpret_cast<u32x2_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4) + (lane >> 5) * 8) = w;
-      }
-  }
-  // Rows are private to the wave: only the wave's own LDS writes must land.
-  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-  constexpr int RPI = 64 / CPR;                  // rows per store instruction
-  uint16_t* cblk = a.C + static_cast<int64_t>(row0 + wm * S::WM) * a.ldc + col0 + wn * S::WN;
-#pragma unroll
-  for (int r0 = 0; r0 < S::WM; r0 += RPI) {
-    const int r = r0 + lane / CPR, c = lane % CPR;
-    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4));
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(cblk + static_cast<int64_t>(r) * a.ldc + c * 8));
-  }
+  char* const cst = sC + wave * (32 * ROWB);     // 32 rows per wave
+  static_assert(4 * 32 * ROWB <= S::C_BYTES, "C staging fits");
 
-  if (a.flags != nullptr) {
-    __syncthreads();
-    if (tid == 0) {
-      const int tiles_n = a.N / kTile;
-      release_fence();
+  int g = 0;
+  for (int lb = 0; lb < mine; ++lb) {
+    const BlockPos bp = block_of_position(a.order, w + lb * G, grid);
 #pragma unroll
-      for (int ti = 0; ti < BM / kTile; ++ti)
+    for (int i = 0; i < S::FM; ++i)
 #pragma unroll
-        for (int tj = 0; tj < BN / kTile; ++tj)
-          publish_relaxed(a.flags + (bp.mb * (BM / kTile) + ti) * tiles_n + bp.nb * (BN / kTile) + tj,
-                          a.epoch);
+      for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    for (int kt = 0; kt < nk; ++kt) step(g++);
+
+    // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
+    // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T): 4
+    // consecutive columns of one row per group of 4 registers.  Each wave
+    // stages 32 rows of its (BM/2) x (BN/2) sub-block at a time in its own
+    // LDS area (16-byte chunks XOR-swizzled by row), then stores whole rows
+    // with 16-byte lanes, so every store instruction writes full 128-byte
+    // lines.  The stores are non-temporal: the partial is read once, by the
+    // reducer, and streaming it past L2 leaves little dirty data for the
+    // release fence to write back.
+    uint16_t* cblk = a.C + static_cast<int64_t>(bp.mb * BM + wm * S::WM) * a.ldc + bp.nb * BN + wn * S::WN;
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i) {
+      const int r = lane & 31;
+#pragma unroll
+      for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = 4 * j + q;               // chunk of columns 32 j + 8 q .. + 7
+          u32x2_t v2;
+          v2[0] = pack_bf16x2(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
+          v2[1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          *reinterpret_cast<u32x2_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4) + (lane >> 5) * 8) = v2;
+        }
+      // The staged rows are private to the wave; LDS operations of one wave
+      // complete in order, so the reads below see the writes above.
+      constexpr int RPI = 64 / CPR;              // rows per store instruction
+#pragma unroll
+      for (int r0 = 0; r0 < 32; r0 += RPI) {
+        const int rr = r0 + lane / CPR, c = lane % CPR;
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + rr * ROWB + ((c ^ (rr % CPR)) << 4));
+        __builtin_nontemporal_store(
+            v, reinterpret_cast<u32x4_t*>(cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8));
+      }
+    }
+
+    if (a.flags != nullptr) {
+      __syncthreads();
+      if (tid == 0) {
+        const int tiles_n = a.N / kTile;
+        release_fence();
+#pragma unroll
+        for (int ti = 0; ti < BM / kTile; ++ti)
+#pragma unroll
+          for (int tj = 0; tj < BN / kTile; ++tj)
+            publish_relaxed(a.flags + (bp.mb * (BM / kTile) + ti) * tiles_n + bp.nb * (BN / kTile) + tj,
+                            a.epoch);
+      }
     }
   }
 }

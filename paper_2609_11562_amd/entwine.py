@@ -37,7 +37,8 @@ class Config(ctypes.Structure):
     _fields_ = [("order", ctypes.c_int32), ("gemm_cfg", ctypes.c_int32),
                 ("reduce_wgs", ctypes.c_int32), ("reduce_threads", ctypes.c_int32),
                 ("timeout_us", ctypes.c_int32), ("withhold_peer", ctypes.c_int32),
-                ("record_timing", ctypes.c_int32), ("group_m", ctypes.c_int32)]
+                ("record_timing", ctypes.c_int32), ("group_m", ctypes.c_int32),
+                ("gemm_wgs", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
     @classmethod
     def make(cls, **kw) -> "Config":
