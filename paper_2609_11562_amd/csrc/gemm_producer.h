@@ -186,34 +186,63 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
 
   // DMA cursor: the next slab of the stream to load (block d_lb, slab d_kt).
   int d_g = 0, d_kt = 0, d_lb = 0;
-  BlockPos d_bp = block_of_position(a.order, w, grid);
-  auto dma_next = [&]() {
+  auto uniform_block = [&](int p) {
+    BlockPos b = block_of_position(a.order, p, grid);
+    b.mb = __builtin_amdgcn_readfirstlane(b.mb);
+    b.nb = __builtin_amdgcn_readfirstlane(b.nb);
+    return b;
+  };
+  BlockPos d_bp = uniform_block(w);
+  struct DmaSlab {
+    const char* Ab;
+    const char* Bb;
+    uint32_t la, lb;
+    int k0;
+    bool whole;   // the slab lies entirely inside K
+  };
+  auto dma_prep = [&]() {
+    DmaSlab d;
     const int st = d_g & 3;
-    const int k0 = d_kt * S::BK;
-    const char* Ab = reinterpret_cast<const char*>(a.A + static_cast<int64_t>(d_bp.mb * BM) * a.lda + k0);
-    const char* Bb = reinterpret_cast<const char*>(a.B + static_cast<int64_t>(k0) * a.ldb + d_bp.nb * BN);
-    const uint32_t la = lds_u32(sA + st * S::A_STAGE + wave * S::A_DMA * 1024);
-    const uint32_t lb = lds_u32(sB + st * S::B_STAGE + wave * S::B_DMA * 1024);
-    if (k0 + S::BK <= K) {                      // whole slab inside K
+    d.k0 = d_kt * S::BK;
+    d.Ab = reinterpret_cast<const char*>(a.A + static_cast<int64_t>(d_bp.mb * BM) * a.lda + d.k0);
+    d.Bb = reinterpret_cast<const char*>(a.B + static_cast<int64_t>(d.k0) * a.ldb + d_bp.nb * BN);
+    d.la = lds_u32(sA + st * S::A_STAGE + wave * S::A_DMA * 1024);
+    d.lb = lds_u32(sB + st * S::B_STAGE + wave * S::B_DMA * 1024);
+    d.whole = d.k0 + S::BK <= K;
+    return d;
+  };
+  // Load i of a whole slab (i < A_DMA: A, else B).
+  auto dma_issue = [&](const DmaSlab& d, int i) {
+    if (i < S::A_DMA) dma16_s(d.Ab, a_off[i], d.la + i * 1024);
+    else dma16_s(d.Bb, b_off[i - S::A_DMA], d.lb + (i - S::A_DMA) * 1024);
+  };
+  // A slab that crosses K: lanes past K read zeros.
+  auto dma_tail = [&](const DmaSlab& d) {
 #pragma unroll
-      for (int i = 0; i < S::A_DMA; ++i) dma16_s(Ab, a_off[i], la + i * 1024);
+    for (int i = 0; i < S::A_DMA; ++i)
+      dma16((d.k0 + a_k[i] < K) ? static_cast<const void*>(d.Ab + a_off[i]) : static_cast<const void*>(a.zeros),
+            d.la + i * 1024);
 #pragma unroll
-      for (int i = 0; i < S::B_DMA; ++i) dma16_s(Bb, b_off[i], lb + i * 1024);
-    } else {                                    // K tail: lanes past K read zeros
-#pragma unroll
-      for (int i = 0; i < S::A_DMA; ++i)
-        dma16((k0 + a_k[i] < K) ? static_cast<const void*>(Ab + a_off[i]) : static_cast<const void*>(a.zeros),
-              la + i * 1024);
-#pragma unroll
-      for (int i = 0; i < S::B_DMA; ++i)
-        dma16((k0 + b_k[i] < K) ? static_cast<const void*>(Bb + b_off[i]) : static_cast<const void*>(a.zeros),
-              lb + i * 1024);
-    }
+    for (int i = 0; i < S::B_DMA; ++i)
+      dma16((d.k0 + b_k[i] < K) ? static_cast<const void*>(d.Bb + b_off[i]) : static_cast<const void*>(a.zeros),
+            d.lb + i * 1024);
+  };
+  auto dma_advance = [&]() {
     ++d_g;
     if (++d_kt == nk) {
       d_kt = 0;
-      if (++d_lb < mine) d_bp = block_of_position(a.order, w + d_lb * G, grid);
+      if (++d_lb < mine) d_bp = uniform_block(w + d_lb * G);
     }
+  };
+  auto dma_next = [&]() {   // a whole slab, not interleaved (prologue)
+    const DmaSlab d = dma_prep();
+    if (d.whole) {
+#pragma unroll
+      for (int i = 0; i < S::DMA; ++i) dma_issue(d, i);
+    } else {
+      dma_tail(d);
+    }
+    dma_advance();
   };
 
   // ---- per-lane LDS read offsets (bytes, relative to a stage)
@@ -238,45 +267,75 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
     bf16x8_t a[S::FM];
     bf16x8_t b[S::FN];
   };
-  auto read_half = [&](Frags& f, int st, auto KK) {
-    constexpr int kk = decltype(KK)::value;
-    const char* As = sA + st * S::A_STAGE + (kk ? a_rd1 : a_rd0);
-    const char* Bs = sB + st * S::B_STAGE + b_row + 16 * kk * S::B_ROW;
-#pragma unroll
-    for (int i = 0; i < S::FM; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(As + i * 32 * 64);
-#pragma unroll
-    for (int j = 0; j < S::FN; ++j) {
-      const bf16x4_t lo = ds_read_tr(Bs + b_col[j]);
-      const bf16x4_t hi = ds_read_tr(Bs + 4 * S::B_ROW + b_col[j]);
+  constexpr int NREAD = S::FM + S::FN;       // LDS read ops per half
+  // Read op r of a half: r < FM reads A fragment r; the others read both
+  // 4-k halves of one B fragment.
+  auto read_one = [&](Frags& f, int st, int kk, int r) {
+    if (r < S::FM) {
+      f.a[r] = *reinterpret_cast<const bf16x8_t*>(sA + st * S::A_STAGE + (kk ? a_rd1 : a_rd0) + r * 32 * 64);
+    } else {
+      const int j = r - S::FM;
+      const char* p = sB + st * S::B_STAGE + b_row + 16 * kk * S::B_ROW + b_col[j];
+      const bf16x4_t lo = ds_read_tr(p);
+      const bf16x4_t hi = ds_read_tr(p + 4 * S::B_ROW);
       f.b[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
   };
-
-  f32x16_t acc[S::FM][S::FN];
-  auto mfma_half = [&](const Frags& f) {
+  auto read_half = [&](Frags& f, int st, int kk) {
 #pragma unroll
-    for (int i = 0; i < S::FM; ++i)
-#pragma unroll
-      for (int j = 0; j < S::FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+    for (int r = 0; r < NREAD; ++r) read_one(f, st, kk, r);
   };
 
-  // One slab g of the stream.  On entry X holds the first K-half of slab g.
-  // Read the second half into Y and multiply X; then make slab g+1 visible
-  // (own loads done, barrier - which also frees the stage of slab g-1), read
-  // its first half into X, queue the loads of slab g+3 into the freed stage,
-  // and multiply Y.  The wait and barrier are unconditional so that every
-  // path reaches the MFMAs with its operands complete.
+  f32x16_t acc[S::FM][S::FN];
+  constexpr int NMF = S::FM * S::FN;         // MFMAs per half
+  auto mfma_one = [&](const Frags& f, int m) {
+    const int i = m / S::FN, j = m % S::FN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+  };
+
+  // One slab g of the stream; on entry X holds the first K-half of slab g.
+  //  phase A: the MFMAs of X, with the LDS reads of the second half (Y)
+  //           spread between them;
+  //  then:    own loads of slab g+1 done, barrier (slab g+1 visible to the
+  //           whole workgroup, and the stage of slab g-1 free again);
+  //  phase B: the MFMAs of Y, with the reads of slab g+1's first half (X)
+  //           and the loads of slab g+3 (into the freed stage) spread
+  //           between them.
+  // sched_barrier pins the interleaving so the matrix core always has the
+  // next MFMA queued while the other instructions issue.
   Frags X, Y;
   auto step = [&](int g) {
-    read_half(Y, g & 3, IC<1>{});
-    mfma_half(X);
+    const int st = g & 3;
+#pragma unroll
+    for (int m = 0; m < NMF; ++m) {
+      mfma_one(X, m);
+#pragma unroll
+      for (int r = m * NREAD / NMF; r < (m + 1) * NREAD / NMF; ++r) read_one(Y, st, 1, r);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (g + 2 < total) wait_vm<S::DMA>();
     else wait_vm<0>();
     __syncthreads();
-    if (g + 1 < total) read_half(X, (g + 1) & 3, IC<0>{});
-    if (g + 3 < total) dma_next();
-    mfma_half(Y);
+    // The next half is always read (past the end of the stream it is a
+    // harmless read of a free stage); the loads of slab g+3 are skipped past
+    // the end, and a slab that crosses K is issued before the MFMAs.
+    const int nst = (g + 1) & 3;
+    const bool ld = g + 3 < total;
+    const DmaSlab d = dma_prep();
+    const bool ld_whole = ld && d.whole;
+    if (ld && !d.whole) dma_tail(d);
+    constexpr int NOPS = NREAD + S::DMA;
+#pragma unroll
+    for (int m = 0; m < NMF; ++m) {
+      mfma_one(Y, m);
+#pragma unroll
+      for (int o = m * NOPS / NMF; o < (m + 1) * NOPS / NMF; ++o) {
+        if (o < NREAD) read_one(X, nst, 0, o);
+        else if (ld_whole) dma_issue(d, o - NREAD);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (ld) dma_advance();
   };
 
   dma_next();
@@ -286,7 +345,7 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   else if (total > 1) wait_vm<S::DMA>();
   else wait_vm<0>();
   __syncthreads();
-  read_half(X, 0, IC<0>{});
+  read_half(X, 0, 0);
 
   constexpr int CPR = S::WN / 8;                 // 16-byte chunks per staged row
   constexpr int ROWB = S::WN * 2;                // bytes per staged row
