@@ -163,13 +163,18 @@ entwine_status check_matrix(entwine_ctx* ctx, const void* p, int64_t ld, int64_t
   } while (0)
 
 typedef void (*GemmKernel)(GemmArgs);
-GemmKernel gemm_kernel(int cfg) {
+template <bool TAIL>
+GemmKernel gemm_kernel_t(int cfg) {
   switch (cfg) {
-    case 0: return gemm_producer<256, 256>;
-    case 1: return gemm_producer<256, 128>;
-    case 2: return gemm_producer<128, 256>;
-    default: return gemm_producer<128, 128>;
+    case 0: return gemm_producer<256, 256, TAIL>;
+    case 1: return gemm_producer<256, 128, TAIL>;
+    case 2: return gemm_producer<128, 256, TAIL>;
+    default: return gemm_producer<128, 128, TAIL>;
   }
+}
+// The tail variant handles K % 32 != 0 (slab width of the producer).
+GemmKernel gemm_kernel(int cfg, int64_t K) {
+  return K % GemmShape<128, 128>::BK ? gemm_kernel_t<true>(cfg) : gemm_kernel_t<false>(cfg);
 }
 
 typedef void (*ReduceKernel)(ReduceArgs);
@@ -250,7 +255,7 @@ entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, i
   g.group_m = r.group_m;
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
-  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg), dim3(producer_grid(ctx, r, fused)), dim3(256), 0, s, g);
+  hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg, ctx->K), dim3(producer_grid(ctx, r, fused)), dim3(256), 0, s, g);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }

@@ -3,8 +3,8 @@
 // Section 4.2).
 //
 // Producer: every thread stores its part of the tile, the workgroup
-// synchronises, then one thread writes the tile's flag with a release store,
-// so the flag is ordered after the stores of the whole workgroup.
+// synchronises, then one thread issues a release fence and writes the tile's
+// flag, so the flag is ordered after the stores of the whole workgroup.
 // Consumer: one thread polls the local flag, then each peer flag, then issues
 // an acquire fence and the workgroup synchronises, which orders every
 // thread's reads of the tile after the producers' stores.
@@ -25,13 +25,16 @@
 
 namespace entwine {
 
-__device__ __forceinline__ void publish_release(int* flag, uint32_t epoch) {
-  __hip_atomic_store(flag, static_cast<int>(epoch), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // Release fence once, then relaxed stores: one L2 write-back covers every
-// flag a producer block publishes.
-__device__ __forceinline__ void release_fence() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+// flag a producer block publishes.  The wait for this wave's outstanding
+// memory operations that the fence implies is also issued explicitly: the
+// producer's tile stores and operand loads are inline asm, which the
+// compiler's wait tracking does not see, so it would drop the fence's own
+// wait as redundant and let a flag overtake the data it publishes.
+__device__ __forceinline__ void release_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __builtin_amdgcn_s_waitcnt(0);   // vmcnt, expcnt and lgkmcnt all zero
+}
 
 __device__ __forceinline__ void publish_relaxed(int* flag, uint32_t epoch) {
   __hip_atomic_store(flag, static_cast<int>(epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

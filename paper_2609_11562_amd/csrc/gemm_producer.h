@@ -2,20 +2,31 @@
 // workgroups take their output blocks in a chosen traversal order and
 // publish a ready flag per 128 x 128 tile (paper Sections 3.1 and 4.2).
 //
-// One workgroup computes a BM x BN block of C = A B (A: M x K, B: K x N, both
+// One workgroup computes BM x BN blocks of C = A B (A: M x K, B: K x N, both
 // row-major bf16) with 4 waves in a 2 x 2 arrangement; each wave owns a
 // (BM/2) x (BN/2) sub-block held as 32 x 32 MFMA accumulators
-// (v_mfma_f32_32x32x16_bf16: fp32 accumulate, 16 K per instruction).
+// (v_mfma_f32_32x32x16_bf16: fp32 accumulate, 16 K per instruction).  The
+// kernel is persistent: workgroup w of G takes logical positions w, w + G,
+// w + 2G, ... and streams all their K-slabs as one sequence.
 //
-// Data path per K-slab of 32:
+// Data path, per K-slab of 32 (two MFMA K-steps of 16):
 //  * global -> LDS with direct-to-LDS loads (global_load_lds_dwordx4): each
 //    instruction moves 64 lanes x 16 bytes into 1 KB of contiguous LDS, no
-//    registers involved.  A slab lives in one of 4 LDS stages; the loads for
-//    slab k+3 are issued while slab k is being multiplied.
+//    registers involved.  Slabs rotate through 4 LDS stages.
+//  * The texture path of a CU accepts roughly one such load per 16 cycles,
+//    so a burst of loads stalls the wave that issues them (and with it the
+//    matrix core).  Each wave's loads of a slab are therefore spread evenly
+//    over two K-steps of MFMAs: slab s + 3 is loaded, half in the last K-step
+//    of slab s - 1 and half in the first K-step of slab s, into the stage
+//    that slab s - 1 has just released.  A slab's loads are issued at least
+//    two slabs before it is read.
+//  * One workgroup barrier per slab, before its last K-step: by then every
+//    wave has read all of the slab's operands into registers (its stage is
+//    free) and its own loads of the next slab have landed.
 //  * LDS layouts are chosen for conflict-free operand reads, and realised by
 //    permuting which global 16-byte chunk each lane fetches:
 //      A stage: [BM rows][32 k] (64-byte rows), chunk c of row r stored at
-//               chunk c ^ ((r >> 2) & 3);
+//               chunk c ^ (((r >> 1) ^ (r >> 3)) & 3);
 //      B stage: [32 k][BN n] (row-major, as in memory), chunk c of row k
 //               stored at chunk c ^ (4 (k & 3)).
 //  * A operands: one ds_read_b128 per 32 x 16 fragment (8 consecutive k per
@@ -24,15 +35,17 @@
 //    4 x 16 blocks across each group of 16 lanes (lane i receives element
 //    i % 4 of the 8 bytes addressed by lane 4e + i / 4, for e = 0..3), so two
 //    such reads build one fragment with no register shuffles.
-//  * Operand fragments of slab k+1 are read from LDS before the MFMAs of
-//    slab k are issued (double-buffered in registers).
-// The K tail (K % 32) is handled without branches: lanes whose 16-byte chunk
-// lies beyond K fetch from a zero page instead.
+//  * Operand fragments of the next K-step are read from LDS between the
+//    first MFMAs of the current one (two register buffers), in the order the
+//    MFMAs consume them.
+// The K tail (K % 32) goes through the same loads with a per-lane address:
+// lanes whose 16-byte chunk lies beyond K fetch from a zero page instead.
 //
 // Epilogue: the MFMA is issued with the B fragment as its first operand, so
 // each lane ends up holding 4 consecutive N values of one output row; they
-// are rounded to bf16 (nearest even) and stored 8 bytes at a time.  Then the
-// workgroup synchronises and one thread publishes the block's tile flags.
+// are rounded to bf16 (nearest even), staged through LDS and stored as whole
+// rows.  Then the workgroup synchronises and one thread publishes the
+// block's tile flags after a release fence.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -68,21 +81,28 @@ struct GemmArgs {
 template <int BM_, int BN_>
 struct GemmShape {
   static constexpr int BM = BM_, BN = BN_;
-  static constexpr int BK = 32;
+  static constexpr int BK = 32;                      // K per slab
+  static constexpr int Q = BK / 16;                  // MFMA K-steps per slab
   static constexpr int THREADS = 256;
-  static constexpr int STAGES = 4;
   static constexpr int WM = BM / 2, WN = BN / 2;     // wave sub-block
   static constexpr int FM = WM / 32, FN = WN / 32;   // 32 x 32 MFMA blocks per wave
-  static constexpr int A_STAGE = BM * BK * 2;        // bytes
-  static constexpr int B_STAGE = BK * BN * 2;
+  static constexpr int A_ROW = BK * 2;               // bytes per LDS row of A
+  static constexpr int B_ROW = BN * 2;               // bytes per LDS row of B
+  static constexpr int A_STAGE = BM * A_ROW;
+  static constexpr int B_STAGE = BK * B_ROW;
+  static constexpr int STAGE = A_STAGE + B_STAGE;    // one slab: A part, then B part
+  static constexpr int STAGES = 4;
+  static constexpr int ROWB = WN * 2;                // bytes per staged C row
+  static constexpr int C_BYTES = 4 * 32 * ROWB;      // epilogue staging, 32 rows per wave
+  static constexpr int LDS_BYTES = STAGES * STAGE + C_BYTES;
   static constexpr int A_DMA = A_STAGE / 1024 / 4;   // 1 KB loads per wave per slab
   static constexpr int B_DMA = B_STAGE / 1024 / 4;
   static constexpr int DMA = A_DMA + B_DMA;
-  static constexpr int B_ROW = BN * 2;               // bytes per LDS row of B
+  static constexpr int DH = DMA / 2;                 // loads per half slab
   static constexpr int B_CPR = BN / 8;               // 16-byte chunks per B row
-  static constexpr int C_BYTES = 32 * 1024;           // epilogue staging, 8 KB per wave
-  static constexpr int LDS_BYTES = STAGES * (A_STAGE + B_STAGE) + C_BYTES;
   static_assert(BM % 128 == 0 && BN % 128 == 0, "blocks are whole 128 x 128 tiles");
+  static_assert(Q == 2 && DMA % 2 == 0, "two K-steps per slab, loads split in halves");
+  static_assert(LDS_BYTES <= 160 * 1024, "gfx950 LDS per workgroup");
 };
 
 template <int V>
@@ -112,11 +132,16 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
   return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-// The base usually arrives through v_readfirstlane (a VALU write of an
-// SGPR); GFX9 needs 5 wait states between that and a VMEM instruction
-// reading the SGPR, which also covers the M0 wait state above.
+// The base may arrive through v_readfirstlane (a VALU write of an SGPR), and
+// GFX9 needs 5 wait states between that and a VMEM instruction reading the
+// SGPR.  The asm therefore copies the base into fresh SGPRs with a scalar
+// move (a scalar write is not subject to that rule) and loads through the
+// copy; the move also provides the wait state after the write of M0.
 __device__ __forceinline__ void dma16_s(const void* base, uint32_t off, uint32_t lds) {
-  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(uniform_ptr(base)), "{m0}"(lds)
+  uint64_t tmp;
+  asm volatile("s_mov_b64 %0, %2\n\tglobal_load_lds_dwordx4 %1, %0"
+               : "=&s"(tmp)
+               : "v"(off), "s"(uniform_ptr(base)), "{m0}"(lds)
                : "memory");
 }
 
@@ -124,6 +149,14 @@ template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Orders LDS accesses between the lanes of one wave (release, wave barrier,
+// acquire at wavefront scope).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -138,14 +171,48 @@ __device__ __forceinline__ bf16x4_t ds_read_tr(const char* p) {
   return __builtin_bit_cast(bf16x4_t, v);
 }
 
-template <int BM, int BN>
+template <int N>
+__device__ __forceinline__ void wait_slabs_le(int n) {
+  // Wait until at most n slabs (n * N loads of this wave) are outstanding.
+  switch (n) {
+    case 0: wait_vm<0>(); break;
+    case 1: wait_vm<N>(); break;
+    default: wait_vm<2 * N>(); break;
+  }
+}
+
+template <int D, int DH>
+__device__ __forceinline__ void wait_loads_le(int n) {
+  // Wait until at most n loads of this wave are outstanding, n a multiple of
+  // DH no larger than 2 D + DH.
+  if (n >= 2 * D + DH) wait_vm<2 * D + DH>();
+  else if (n >= 2 * D) wait_vm<2 * D>();
+  else if (n >= D + DH) wait_vm<D + DH>();
+  else if (n >= D) wait_vm<D>();
+  else if (n >= DH) wait_vm<DH>();
+  else wait_vm<0>();
+}
+
+// Store 16 bytes with system scope (sc0 sc1): the data is written through
+// the L2 instead of being left dirty in it, so the release fence that
+// publishes a tile has little to write back.  The trailing wait state covers
+// the hazard of a VALU write to the store's data registers right after a
+// store of more than 8 bytes (the compiler does not insert it for asm).
+__device__ __forceinline__ void store16_wt(void* dst, u32x4_t v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1\n\ts_nop 0" ::"v"(dst), "v"(v) : "memory");
+}
+
+// TAIL: K % 32 != 0.  Without a tail every slab is whole, so the loads are
+// issued unconditionally: past the end of the stream they re-read the last
+// slab (valid memory) into the stage that is free at that point, which no
+// real slab uses again; they are drained before the kernel ends.
+template <int BM, int BN, bool TAIL>
 __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   using S = GemmShape<BM, BN>;
-  // LDS: 4 A stages, 4 B stages, then a C staging area (8 KB per wave).
+  constexpr int NS = S::STAGES;
+  constexpr int D = S::DMA, DH = S::DH;
+  static_assert(2 * D + DH < 64, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char smem[S::LDS_BYTES];
-  char* const sA = smem;
-  char* const sB = smem + 4 * S::A_STAGE;
-  char* const sC = smem + 4 * (S::A_STAGE + S::B_STAGE);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -165,13 +232,16 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   const int total = mine * nk;
   if (total == 0) return;
 
-  // ---- per-lane DMA sources: byte offsets inside a block, and their K
+  // ---- per-lane load sources: byte offsets inside a block, and their K.
+  // A: one load fills 16 rows of 64 bytes; lane -> row lane / 4, stored
+  // chunk lane % 4, which holds logical chunk (lane % 4) ^ sw(row).
+  // B: one load fills 1 KB of consecutive [k][n] rows.
   uint32_t a_off[S::A_DMA], b_off[S::B_DMA];
   int a_k[S::A_DMA], b_k[S::B_DMA];
 #pragma unroll
   for (int i = 0; i < S::A_DMA; ++i) {
     const int r = (wave * S::A_DMA + i) * 16 + (lane >> 2);
-    const int lc = (lane & 3) ^ ((r >> 2) & 3);
+    const int lc = (lane & 3) ^ (((r >> 1) ^ (r >> 3)) & 3);
     a_off[i] = static_cast<uint32_t>((r * a.lda + lc * 8) * 2);
     a_k[i] = lc * 8;
   }
@@ -184,77 +254,93 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
     b_k[i] = r;
   }
 
-  // DMA cursor: the next slab of the stream to load (block d_lb, slab d_kt).
-  int d_g = 0, d_kt = 0, d_lb = 0;
+  // ---- load cursor: the slab being loaded (block d_lb, slab d_kt of it),
+  // with wave-uniform base addresses advanced incrementally.
   auto uniform_block = [&](int p) {
     BlockPos b = block_of_position(a.order, p, grid);
     b.mb = __builtin_amdgcn_readfirstlane(b.mb);
     b.nb = __builtin_amdgcn_readfirstlane(b.nb);
     return b;
   };
+  auto a_base = [&](const BlockPos& b) {
+    return reinterpret_cast<const char*>(a.A + static_cast<int64_t>(b.mb * BM) * a.lda);
+  };
+  auto b_base = [&](const BlockPos& b) { return reinterpret_cast<const char*>(a.B + b.nb * BN); };
+  int d_g = 0, d_kt = 0, d_lb = 0;
   BlockPos d_bp = uniform_block(w);
-  struct DmaSlab {
-    const char* Ab;
-    const char* Bb;
-    uint32_t la, lb;
-    int k0;
-    bool whole;   // the slab lies entirely inside K
+  const char* dA = a_base(d_bp);
+  const char* dB = b_base(d_bp);
+  const int64_t b_step = static_cast<int64_t>(S::BK) * a.ldb * 2;   // bytes per slab of B
+  static_assert((NS & (NS - 1)) == 0, "stage index by mask");
+  auto st_base = [&](int g) { return smem + (g & (NS - 1)) * S::STAGE; };
+  auto la_of = [&](int g) { return lds_u32(st_base(g) + wave * S::A_DMA * 1024); };
+  auto lb_of = [&](int g) { return lds_u32(st_base(g) + S::A_STAGE + wave * S::B_DMA * 1024); };
+  auto d_whole = [&]() { return (d_kt + 1) * S::BK <= K; };
+  // Load o (0 <= o < D) of the cursor's slab, which lies inside K: o < A_DMA
+  // from A, else from B.
+  auto dma_issue = [&](uint32_t la, uint32_t lb, int o) {
+    if (o < S::A_DMA) dma16_s(dA, a_off[o], la + o * 1024);
+    else dma16_s(dB, b_off[o - S::A_DMA], lb + (o - S::A_DMA) * 1024);
   };
-  auto dma_prep = [&]() {
-    DmaSlab d;
-    const int st = d_g & 3;
-    d.k0 = d_kt * S::BK;
-    d.Ab = reinterpret_cast<const char*>(a.A + static_cast<int64_t>(d_bp.mb * BM) * a.lda + d.k0);
-    d.Bb = reinterpret_cast<const char*>(a.B + static_cast<int64_t>(d.k0) * a.ldb + d_bp.nb * BN);
-    d.la = lds_u32(sA + st * S::A_STAGE + wave * S::A_DMA * 1024);
-    d.lb = lds_u32(sB + st * S::B_STAGE + wave * S::B_DMA * 1024);
-    d.whole = d.k0 + S::BK <= K;
-    return d;
-  };
-  // Load i of a whole slab (i < A_DMA: A, else B).
-  auto dma_issue = [&](const DmaSlab& d, int i) {
-    if (i < S::A_DMA) dma16_s(d.Ab, a_off[i], d.la + i * 1024);
-    else dma16_s(d.Bb, b_off[i - S::A_DMA], d.lb + (i - S::A_DMA) * 1024);
-  };
-  // A slab that crosses K: lanes past K read zeros.
-  auto dma_tail = [&](const DmaSlab& d) {
+  // Loads [o0, o1) of the cursor's slab, which crosses K: lanes past K read zeros.
+  auto dma_tail = [&](uint32_t la, uint32_t lb, int o0, int o1) {
+    const int k0 = d_kt * S::BK;
 #pragma unroll
-    for (int i = 0; i < S::A_DMA; ++i)
-      dma16((d.k0 + a_k[i] < K) ? static_cast<const void*>(d.Ab + a_off[i]) : static_cast<const void*>(a.zeros),
-            d.la + i * 1024);
-#pragma unroll
-    for (int i = 0; i < S::B_DMA; ++i)
-      dma16((d.k0 + b_k[i] < K) ? static_cast<const void*>(d.Bb + b_off[i]) : static_cast<const void*>(a.zeros),
-            d.lb + i * 1024);
+    for (int o = 0; o < D; ++o) {
+      if (o < o0 || o >= o1) continue;
+      if (o < S::A_DMA) {
+        dma16((k0 + a_k[o] < K) ? static_cast<const void*>(dA + a_off[o]) : static_cast<const void*>(a.zeros),
+              la + o * 1024);
+      } else {
+        const int i = o - S::A_DMA;
+        dma16((k0 + b_k[i] < K) ? static_cast<const void*>(dB + b_off[i]) : static_cast<const void*>(a.zeros),
+              lb + i * 1024);
+      }
+    }
   };
+  // Loads [o0, o1) of the cursor's slab, not interleaved with MFMAs.
+  auto dma_range = [&](int o0, int o1) {
+    const uint32_t la = la_of(d_g), lb = lb_of(d_g);
+    if (!TAIL || d_whole()) {
+#pragma unroll
+      for (int o = 0; o < D; ++o)
+        if (o >= o0 && o < o1) dma_issue(la, lb, o);
+    } else {
+      dma_tail(la, lb, o0, o1);
+    }
+  };
+  // Past the last slab the cursor stays on it.
   auto dma_advance = [&]() {
     ++d_g;
+    if (d_lb == mine) return;
     if (++d_kt == nk) {
-      d_kt = 0;
-      if (++d_lb < mine) d_bp = uniform_block(w + d_lb * G);
-    }
-  };
-  auto dma_next = [&]() {   // a whole slab, not interleaved (prologue)
-    const DmaSlab d = dma_prep();
-    if (d.whole) {
-#pragma unroll
-      for (int i = 0; i < S::DMA; ++i) dma_issue(d, i);
+      if (++d_lb < mine) {
+        d_kt = 0;
+        d_bp = uniform_block(w + d_lb * G);
+        dA = a_base(d_bp);
+        dB = b_base(d_bp);
+      } else {
+        d_kt = nk - 1;
+      }
     } else {
-      dma_tail(d);
+      dA += S::BK * 2;
+      dB += b_step;
     }
-    dma_advance();
   };
 
   // ---- per-lane LDS read offsets (bytes, relative to a stage)
-  // A fragment (rows wm*WM + i*32 + lane%32, 8 k per lane at 16 kk + 8 (lane/32)).
+  // A fragment i of K-step q: rows wm*WM + 32 i + lane % 32, 8 consecutive k
+  // at 16 q + 8 (lane / 32), i.e. logical chunk 2 q + lane / 32.
   const int a_row = wm * S::WM + (lane & 31);
-  const int a_rd0 = a_row * 64 + (((lane >> 5) ^ ((a_row >> 2) & 3)) << 4);
-  const int a_rd1 = a_row * 64 + (((2 + (lane >> 5)) ^ ((a_row >> 2) & 3)) << 4);
+  const int a_sw = ((a_row >> 1) ^ (a_row >> 3)) & 3;    // same for a_row + 32 i
+  int a_rd[S::Q];
+#pragma unroll
+  for (int q = 0; q < S::Q; ++q) a_rd[q] = a_row * S::A_ROW + (((2 * q + (lane >> 5)) ^ a_sw) << 4);
   // B fragment via transpose reads: lane = 16 g + i; reads row
-  // k = 16 kk + 8 (g / 2) + 4 h + i / 4, columns n .. n+3 with
+  // k = 16 q + 8 (g / 2) + 4 h + i / 4, columns n .. n+3 with
   // n = wn*WN + 32 j + 16 (g % 2) + 4 (i % 4).
   const int b_kq = (lane >> 2) & 3;                       // k & 3 of the row read
-  const int b_row = (8 * (lane >> 5) + b_kq) * S::B_ROW;  // + (16 kk + 4 h) * B_ROW
+  const int b_row = S::A_STAGE + (8 * (lane >> 5) + b_kq) * S::B_ROW;
   int b_col[S::FN];
 #pragma unroll
   for (int j = 0; j < S::FN; ++j) {
@@ -262,95 +348,105 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
     b_col[j] = (((n >> 3) ^ (4 * b_kq)) << 4) + ((n & 7) << 1);
   }
 
-  // Fragments of one K-half (16 k) of a slab.
+  // Fragments of one K-step.
   struct Frags {
     bf16x8_t a[S::FM];
     bf16x8_t b[S::FN];
   };
-  constexpr int NREAD = S::FM + S::FN;       // LDS read ops per half
-  // Read op r of a half: r < FM reads A fragment r; the others read both
-  // 4-k halves of one B fragment.
-  auto read_one = [&](Frags& f, int st, int kk, int r) {
-    if (r < S::FM) {
-      f.a[r] = *reinterpret_cast<const bf16x8_t*>(sA + st * S::A_STAGE + (kk ? a_rd1 : a_rd0) + r * 32 * 64);
+  constexpr int NREAD = S::FM + S::FN;       // LDS read ops per K-step
+  // Read op r of K-step q, in the order the MFMAs consume the fragments:
+  // A fragment 0, the B fragments, then the other A fragments.
+  auto read_one = [&](Frags& f, const char* stg, int q, int r) {
+    if (r == 0 || r > S::FN) {
+      const int i = r == 0 ? 0 : r - S::FN;
+      f.a[i] = *reinterpret_cast<const bf16x8_t*>(stg + a_rd[q] + i * 32 * S::A_ROW);
     } else {
-      const int j = r - S::FM;
-      const char* p = sB + st * S::B_STAGE + b_row + 16 * kk * S::B_ROW + b_col[j];
+      const int j = r - 1;
+      const char* p = stg + b_row + 16 * q * S::B_ROW + b_col[j];
       const bf16x4_t lo = ds_read_tr(p);
       const bf16x4_t hi = ds_read_tr(p + 4 * S::B_ROW);
       f.b[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
   };
-  auto read_half = [&](Frags& f, int st, int kk) {
-#pragma unroll
-    for (int r = 0; r < NREAD; ++r) read_one(f, st, kk, r);
-  };
 
   f32x16_t acc[S::FM][S::FN];
-  constexpr int NMF = S::FM * S::FN;         // MFMAs per half
+  constexpr int NMF = S::FM * S::FN;         // MFMAs per K-step
   auto mfma_one = [&](const Frags& f, int m) {
     const int i = m / S::FN, j = m % S::FN;
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
   };
-
-  // One slab g of the stream; on entry X holds the first K-half of slab g.
-  //  phase A: the MFMAs of X, with the LDS reads of the second half (Y)
-  //           spread between them;
-  //  then:    own loads of slab g+1 done, barrier (slab g+1 visible to the
-  //           whole workgroup, and the stage of slab g-1 free again);
-  //  phase B: the MFMAs of Y, with the reads of slab g+1's first half (X)
-  //           and the loads of slab g+3 (into the freed stage) spread
-  //           between them.
-  // sched_barrier pins the interleaving so the matrix core always has the
-  // next MFMA queued while the other instructions issue.
-  Frags X, Y;
-  auto step = [&](int g) {
-    const int st = g & 3;
+  // One K-step: the MFMAs of `cur`, with the NREAD reads of the next K-step
+  // (into `nxt`, from stage `stg`, K-step qn) after the first NREAD MFMAs,
+  // and loads [o0, o0 + DH) of the cursor's slab (when `ldw`) spread evenly
+  // over all of them.  Reading early leaves the reads complete before the
+  // barrier or the next K-step needs them.  sched_barrier pins the
+  // interleaving so the matrix core always has the next MFMA queued while the
+  // other instructions issue.
+  static_assert(NREAD <= NMF, "one read op per MFMA at most");
+  auto kstep = [&](const Frags& cur, Frags& nxt, const char* stg, int qn, bool ldw, uint32_t la, uint32_t lb,
+                   int o0) {
 #pragma unroll
     for (int m = 0; m < NMF; ++m) {
-      mfma_one(X, m);
+      mfma_one(cur, m);
+      if (m < NREAD) read_one(nxt, stg, qn, m);
 #pragma unroll
-      for (int r = m * NREAD / NMF; r < (m + 1) * NREAD / NMF; ++r) read_one(Y, st, 1, r);
+      for (int k = 0; k < DH; ++k)
+        if (m == (k + 1) * NMF / DH - 1 && (!TAIL || ldw)) dma_issue(la, lb, o0 + k);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (g + 2 < total) wait_vm<S::DMA>();
-    else wait_vm<0>();
-    __syncthreads();
-    // The next half is always read (past the end of the stream it is a
-    // harmless read of a free stage); the loads of slab g+3 are skipped past
-    // the end, and a slab that crosses K is issued before the MFMAs.
-    const int nst = (g + 1) & 3;
-    const bool ld = g + 3 < total;
-    const DmaSlab d = dma_prep();
-    const bool ld_whole = ld && d.whole;
-    if (ld && !d.whole) dma_tail(d);
-    constexpr int NOPS = NREAD + S::DMA;
-#pragma unroll
-    for (int m = 0; m < NMF; ++m) {
-      mfma_one(Y, m);
-#pragma unroll
-      for (int o = m * NOPS / NMF; o < (m + 1) * NOPS / NMF; ++o) {
-        if (o < NREAD) read_one(X, nst, 0, o);
-        else if (ld_whole) dma_issue(d, o - NREAD);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (ld) dma_advance();
   };
 
-  dma_next();
-  if (total > 1) dma_next();
-  if (total > 2) dma_next();
-  if (total > 2) wait_vm<2 * S::DMA>();
-  else if (total > 1) wait_vm<S::DMA>();
-  else wait_vm<0>();
+  // One slab g of the stream; on entry X holds K-step 0 of slab g and the
+  // cursor is at slab g + NS - 1 with its first half issued.
+  //  K-step 0: MFMAs of X; reads of K-step 1 into Y; second half of the
+  //            cursor's slab.
+  //  then:     own loads of slab g+1 done, barrier: slab g+1 is visible to
+  //            the workgroup, and every wave has read all of slab g.
+  //  K-step 1: MFMAs of Y; reads of slab g+1's K-step 0 into X; first half
+  //            of slab g + NS, into slab g's stage (free now).
+  // Past the end of the stream no loads are issued and the reads of the next
+  // K-step are harmless reads of a stage that is not used again.
+  Frags X, Y;
+  auto step = [&](int g) {
+    {
+      const bool ld = !TAIL || g + NS - 1 < total;
+      const bool ldw = !TAIL || (ld && d_whole());
+      const uint32_t la = la_of(d_g), lb = lb_of(d_g);
+      if (TAIL && ld && !ldw) dma_tail(la, lb, DH, D);
+      kstep(X, Y, st_base(g), 1, ldw, la, lb, DH);
+      if (ld) dma_advance();
+    }
+    // slabs issued after g+1 that may still be in flight
+    int after = NS - 2;
+    if (TAIL && total - g - 2 < after) after = total - g - 2 > 0 ? total - g - 2 : 0;
+    wait_slabs_le<D>(after);
+    __syncthreads();
+    {
+      const bool ld = !TAIL || g + NS < total;
+      const bool ldw = !TAIL || (ld && d_whole());
+      const uint32_t la = la_of(d_g), lb = lb_of(d_g);
+      if (TAIL && ld && !ldw) dma_tail(la, lb, 0, DH);
+      kstep(Y, X, st_base(g + 1), 0, ldw, la, lb, 0);
+    }
+  };
+
+  // ---- prologue: slabs 0 .. NS-2 and the first half of slab NS-1 in
+  // flight, slab 0 visible, K-step 0 of slab 0 in X.
+  const int nfull = !TAIL || total >= NS - 1 ? NS - 1 : total;
+  for (int i = 0; i < nfull; ++i) {
+    dma_range(0, D);
+    dma_advance();
+  }
+  const bool half = !TAIL || NS - 1 < total;
+  if (half) dma_range(0, DH);
+  wait_loads_le<D, DH>((nfull - 1) * D + (half ? DH : 0));
   __syncthreads();
-  read_half(X, 0, 0);
+#pragma unroll
+  for (int r = 0; r < NREAD; ++r) read_one(X, st_base(0), 0, r);
 
   constexpr int CPR = S::WN / 8;                 // 16-byte chunks per staged row
-  constexpr int ROWB = S::WN * 2;                // bytes per staged row
-  char* const cst = sC + wave * (32 * ROWB);     // 32 rows per wave
-  static_assert(4 * 32 * ROWB <= S::C_BYTES, "C staging fits");
+  constexpr int ROWB = S::ROWB;
+  char* const cst = smem + NS * S::STAGE + wave * (32 * ROWB);
 
   int g = 0;
   for (int lb = 0; lb < mine; ++lb) {
@@ -365,13 +461,10 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
 
     // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
     // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T): 4
-    // consecutive columns of one row per group of 4 registers.  Each wave
-    // stages 32 rows of its (BM/2) x (BN/2) sub-block at a time in its own
-    // LDS area (16-byte chunks XOR-swizzled by row), then stores whole rows
-    // with 16-byte lanes, so every store instruction writes full 128-byte
-    // lines.  The stores are non-temporal: the partial is read once, by the
-    // reducer, and streaming it past L2 leaves little dirty data for the
-    // release fence to write back.
+    // consecutive columns of one row per group of 4 registers.  32 rows at a
+    // time are staged in this wave's own LDS area (16-byte chunks
+    // XOR-swizzled by row), then stored as whole rows with 16-byte lanes, so
+    // every store instruction writes full 128-byte lines.
     uint16_t* cblk = a.C + static_cast<int64_t>(bp.mb * BM + wm * S::WM) * a.ldc + bp.nb * BN + wn * S::WN;
 #pragma unroll
     for (int i = 0; i < S::FM; ++i) {
@@ -386,16 +479,17 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
           v2[1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
           *reinterpret_cast<u32x2_t*>(cst + r * ROWB + ((c ^ (r % CPR)) << 4) + (lane >> 5) * 8) = v2;
         }
-      // The staged rows are private to the wave; LDS operations of one wave
-      // complete in order, so the reads below see the writes above.
+      // Lanes read rows other lanes wrote: synchronise the wave (lanes are
+      // separate threads to the compiler, which may otherwise move the reads).
+      wave_sync();
       constexpr int RPI = 64 / CPR;              // rows per store instruction
 #pragma unroll
       for (int r0 = 0; r0 < 32; r0 += RPI) {
         const int rr = r0 + lane / CPR, c = lane % CPR;
         const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + rr * ROWB + ((c ^ (rr % CPR)) << 4));
-        __builtin_nontemporal_store(
-            v, reinterpret_cast<u32x4_t*>(cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8));
+        store16_wt(cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8, v);
       }
+      wave_sync();                               // the next round rewrites these rows
     }
 
     if (a.flags != nullptr) {
@@ -412,6 +506,8 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
       }
     }
   }
+  // Loads past the end of the stream may still be writing LDS.
+  if (!TAIL) wait_vm<0>();
 }
 
 }  // namespace entwine

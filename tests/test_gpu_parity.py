@@ -130,6 +130,8 @@ def test_results_independent_of_order_budget_threads_and_mode():
         check_rows(prob, base[::37], np.arange(M)[::37])
         variants = [dict(order=o) for o in (1, 2)] + [dict(gemm_cfg=c) for c in (1, 2, 3)] + \
                    [dict(group_m=g) for g in (1, 2, 8)] + [dict(order=2, group_m=1)] + \
+                   [dict(gemm_wgs=8), dict(gemm_cfg=1, gemm_wgs=24), dict(gemm_cfg=2, gemm_wgs=16),
+                    dict(gemm_cfg=3, gemm_wgs=40)] + \
                    [dict(reduce_wgs=x) for x in (4, 8, 32, 64)] + \
                    [dict(reduce_threads=b) for b in (128, 512)]
         for kw in variants:
