@@ -114,8 +114,9 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
     return fail(ctx, ENTWINE_EINVAL, "dest=%d outside [-1, P)", dest);
   if (c.order < 0 || c.order > 2) return fail(ctx, ENTWINE_EINVAL, "unknown order %d", c.order);
   if (c.gemm_cfg < -1 || c.gemm_cfg >= ENTWINE_GEMM_NUM_CFGS) return fail(ctx, ENTWINE_EINVAL, "unknown gemm_cfg %d", c.gemm_cfg);
-  if (c.reduce_threads != 0 && c.reduce_threads != 128 && c.reduce_threads != 256 && c.reduce_threads != 512)
-    return fail(ctx, ENTWINE_EINVAL, "reduce_threads must be 128, 256 or 512");
+  if (c.reduce_threads != 0 && c.reduce_threads != 128 && c.reduce_threads != 256 && c.reduce_threads != 512 &&
+      c.reduce_threads != 1024)
+    return fail(ctx, ENTWINE_EINVAL, "reduce_threads must be 128, 256, 512 or 1024");
   if (c.reduce_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "reduce_wgs must be >= 0");
   if (c.timeout_us < 0) return fail(ctx, ENTWINE_EINVAL, "timeout_us must be >= 0");
   if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
@@ -194,6 +195,7 @@ ReduceKernel reduce_kernel_p(int P) {
 ReduceKernel reduce_kernel(int threads, int P) {
   if (threads == 128) return reduce_kernel_p<128>(P);
   if (threads == 512) return reduce_kernel_p<512>(P);
+  if (threads == 1024) return reduce_kernel_p<1024>(P);
   return reduce_kernel_p<256>(P);
 }
 

@@ -3,8 +3,9 @@
 // (paper Section 3.1 "Matching task order", Section 4.2 ReduceTile).
 //
 // Workgroup j walks tiles j, j+x, j+2x, ... of its partition in producer
-// order.  For each tile one thread waits for the local flag and then for the
-// P-1 peer flags, issues an acquire fence, and the workgroup synchronises.
+// order.  For each tile, lanes 0 .. P-1 of the first wave poll the local flag
+// and the P-1 peer flags together (one memory round trip per poll instead of
+// P), then one lane issues an acquire fence and the workgroup synchronises.
 // The workgroup then reduces the tile: every element is initialised from the
 // local bf16 contribution, the peer values are added in rank order in fp32,
 // and the result is rounded to bf16 (nearest even) and stored once - each
@@ -13,9 +14,11 @@
 // Data movement: a tile row is 256 bytes = 16 lanes x 16 bytes, so each wave
 // moves 4 full rows per instruction (coalesced).  Contributions are read once
 // and the output written once, so both use non-temporal accesses to keep the
-// producer's A/B panels in cache.  G vectors per contribution are loaded
-// before any is consumed, giving G * P independent 16-byte loads in flight
-// per lane.
+// producer's A/B panels in cache.  A reducer CU is bound by how many bytes it
+// keeps in flight, so each lane issues up to 32 independent 16-byte loads
+// (G vectors of every contribution) before consuming any, and the first poll
+// of the next tile's flags is issued right behind the current tile's loads,
+// so its round trip overlaps theirs.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -54,11 +57,19 @@ __device__ __forceinline__ r_u32x4_t ld_stream(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const r_u32x4_t*>(p));
 }
 
+constexpr int pow2_floor(int v) {
+  int p = 1;
+  while (p * 2 <= v) p *= 2;
+  return p;
+}
+
 template <int THREADS, int NP>
 __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
   constexpr int VPT = (kTile * kTile * 2 / 16) / THREADS;  // 16-byte vectors per thread
-  constexpr int G = (NP >= 6) ? 2 : 4;                      // vectors per batch
+  constexpr int GMAX = 32 / NP;                             // loads in flight per lane <= 32
+  constexpr int G = pow2_floor(VPT < GMAX ? VPT : GMAX);    // vectors per batch
   static_assert(VPT % G == 0, "batch must divide the per-thread vectors");
+  static_assert(NP <= 64, "one polling lane per contribution");
   __shared__ int s_abort;
 
   const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
@@ -67,33 +78,60 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
   const int ntiles = (a.M / kTile) * tiles_n;
   const ConsumerSeq seq = consumer_seq(a.dest, NP, a.x, blockIdx.x);
   const int chunk_rows = a.M / NP;
+  const int lane = threadIdx.x & 63;
+  const bool poller = threadIdx.x < NP;       // lanes 0 .. NP-1 of wave 0
+  const int epoch = static_cast<int>(a.epoch);
 
-  for (int t = seq.first; t < Q; t += seq.stride) {
+  auto global_tile = [&](int t) {
     int tr, tc;
     tile_of_number(seq.part, t, grid, &tr, &tc);
-    const int gt = tr * tiles_n + tc;
-
-    if (threadIdx.x == 0) {
-      const uint64_t deadline = wall_clock64() + a.timeout_ticks;
-      int src = -2;   // -2: all ready, -1: local flag missing, q: peer q missing
-      if (!await_flag(a.flags + gt, a.epoch, deadline)) src = -1;
-      for (int q = 0; q < NP - 1 && src == -2; ++q)
-        if (!await_flag(a.peer_flags + static_cast<int64_t>(q) * ntiles + gt, a.epoch, deadline)) src = q;
-      if (src != -2) {
-        if (atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
+    return tr * tiles_n + tc;
+  };
+  // Flag polled by this lane: lane 0 the local flag, lane q+1 peer q's.
+  auto flag_of = [&](int gt) {
+    return lane == 0 ? a.flags + gt : a.peer_flags + static_cast<int64_t>(lane - 1) * ntiles + gt;
+  };
+  // Wave 0: wait until every flag of tile gt is ready (`seen` holds a first
+  // poll already made), then acquire; returns false, after recording the
+  // timeout, if the deadline passes first.  Called by wave 0 only.
+  auto await_tile = [&](int gt, int seen) {
+    bool ready = !poller || seen == epoch;
+    const uint64_t deadline = wall_clock64() + a.timeout_ticks;
+    while (__ballot(!ready) != 0) {
+      if (wall_clock64() > deadline) {
+        const uint64_t missing = __ballot(!ready);
+        const int first = __builtin_ctzll(missing);
+        if (lane == 0 && atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
           atomicExch(a.status + 1, gt);
-          atomicExch(a.status + 2, src);
+          atomicExch(a.status + 2, first == 0 ? -1 : first - 1);   // -1 local, q peer q
         }
+        return false;
       }
-      acquire_fence();
-      s_abort = (src != -2);
+      __builtin_amdgcn_s_sleep(1);
+      if (!ready) ready = poll_relaxed(flag_of(gt)) == epoch;
     }
-    __syncthreads();
-    if (s_abort) return;
+    if (lane == 0) acquire_fence();
+    return true;
+  };
 
-    const int64_t grow0 = static_cast<int64_t>(tr) * kTile;
-    const int64_t gcol0 = static_cast<int64_t>(tc) * kTile;
+  int t = seq.first;
+  if (t >= Q) return;
+  int gt = global_tile(t);
+  if (threadIdx.x < 64) {
+    const int seen = poller ? poll_relaxed(flag_of(gt)) : epoch;
+    const bool ok = await_tile(gt, seen);
+    if (lane == 0) s_abort = !ok;
+  }
+  __syncthreads();
+  if (s_abort) return;
+
+  while (true) {
+    const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile;
+    const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
     const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * chunk_rows : grow0;
+    const int tn = t + seq.stride;
+    const int gtn = tn < Q ? global_tile(tn) : 0;
+    int seen = epoch;
 
 #pragma unroll
     for (int v0 = 0; v0 < VPT; v0 += G) {
@@ -107,6 +145,8 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
 #pragma unroll
         for (int q = 0; q < NP - 1; ++q) pv[q][gi] = ld_stream(a.peers[q] + (grow0 + r) * a.ldp + gcol0 + cc);
       }
+      // First poll of the next tile's flags, behind the first batch's loads.
+      if (v0 == 0 && poller && tn < Q) seen = poll_relaxed(flag_of(gtn));
 #pragma unroll
       for (int gi = 0; gi < G; ++gi) {
         float acc[8];
@@ -130,7 +170,16 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
         __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc));
       }
     }
-    __syncthreads();   // s_abort is rewritten for the next tile
+    if (tn >= Q) break;
+    t = tn;
+    gt = gtn;
+    __syncthreads();   // s_abort is rewritten below
+    if (threadIdx.x < 64) {
+      const bool ok = await_tile(gt, seen);
+      if (lane == 0) s_abort = !ok;
+    }
+    __syncthreads();
+    if (s_abort) return;
   }
 }
 
