@@ -79,7 +79,8 @@ typedef struct {
                              (Section 3.2); 0 = default; capped at the tile
                              count and at CUs - 1.  With DEST_ALL it is
                              rounded up to a multiple of P. */
-  int32_t reduce_threads; /* b: threads per reducer workgroup, 128/256/512/1024 */
+  int32_t reduce_threads; /* b: threads per reducer workgroup, 128/256/512/1024
+                             (0 = default = 1024) */
   int32_t timeout_us;     /* bound on one reducer wait, microseconds
                              (0 = 2 s); expiry sets ENTWINE_ETIMEOUT */
   int32_t withhold_peer;  /* test hook: peer q whose flags are not published

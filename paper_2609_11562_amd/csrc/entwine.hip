@@ -140,7 +140,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
     x = std::min(std::min(x, Q), cap_cus);
   }
   r->x = std::max(x, 1);
-  r->threads = c.reduce_threads ? c.reduce_threads : 256;
+  r->threads = c.reduce_threads ? c.reduce_threads : 1024;
   r->withhold = c.withhold_peer;
   r->timing = c.record_timing;
   r->timeout_us = c.timeout_us ? uint64_t(c.timeout_us) : 2000000ull;

@@ -1,0 +1,36 @@
+"""Host-only checks of the configuration table (paper Section 4.3: the
+offline profiler's choice of block shape, x and b is looked up per
+workload)."""
+import json
+
+from paper_2609_11562_amd import entwine as E
+from paper_2609_11562_amd import tune, tuning
+from paper_2609_11562_amd.workloads import WORKLOADS
+
+
+def test_table_entries_are_valid_configs():
+    table = tuning.load_table()
+    for name, scopes in table.items():
+        assert name in WORKLOADS, name
+        w = WORKLOADS[name]
+        for scope, entry in scopes.items():
+            assert scope in ("rank", "all")
+            kw = tuning.tuned_config(name, scope)
+            assert set(kw) <= set(tuning._FIELDS) and kw
+            dest = E.DEST_ALL if scope == "all" else 0
+            assert E.validate(w.M, w.N, w.K, w.P, dest, E.Config.make(**kw)) == E.OK
+
+
+def test_missing_workload_falls_back_to_defaults():
+    assert tuning.tuned_config("no_such_workload") == {}
+
+
+def test_write_entry_round_trip(tmp_path):
+    path = tmp_path / "t.json"
+    best = dict(order=0, gemm_cfg=1, reduce_wgs=24, reduce_threads=512, group_m=4, wall_ms=0.5, event_ms=0.4)
+    tune.write_entry("llama7b_mlp_down_tp8", "rank", best, str(path))
+    tune.write_entry("llama7b_mlp_down_tp8", "all", dict(best, reduce_wgs=32), str(path))
+    t = json.loads(path.read_text())
+    assert t["llama7b_mlp_down_tp8"]["rank"]["reduce_wgs"] == 24
+    assert t["llama7b_mlp_down_tp8"]["all"]["reduce_wgs"] == 32
+    assert t["llama7b_mlp_down_tp8"]["rank"]["measured_ms"] == 0.5
