@@ -93,7 +93,13 @@ typedef struct {
                              positions w, w + G, ...): 0 = default = the CUs,
                              minus x in the fused path, rounded down to a
                              multiple of 8 (one workgroup per CU) */
-  int32_t reserved;
+  int32_t launch;         /* fused path (distinct streams): 0 = one kernel
+                             launch on gemm_stream whose first G workgroups
+                             are producers and last x reducers of 256
+                             threads (reduce_threads then does not apply;
+                             G is capped so that all are resident);
+                             1 = two kernels on the two streams (Section
+                             4.3's form), with b threads per reducer */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */

@@ -17,9 +17,11 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "../../include/entwine.h"
 #include "gemm_producer.h"
+#include "gemm_reduce_fused.h"
 #include "tile_order.h"
 #include "tile_reducer.h"
 
@@ -28,10 +30,13 @@ using namespace entwine;
 namespace {
 
 constexpr int kRing = 256;
+constexpr int kStampWgs = 1024;   // workgroups with per-call timestamps (single launch)
 
 struct TimingSlot {
   hipEvent_t start = nullptr, gemm_end = nullptr, red_end = nullptr;
   bool has_gemm = false, has_red = false;
+  bool has_stamps = false;   // single launch: role spans from device timestamps
+  int G = 0, grid = 0;
 };
 
 struct CfgShape {
@@ -56,6 +61,7 @@ struct entwine_ctx {
   uint64_t ticks_per_us = 100;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   TimingSlot ring[kRing];
+  unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, end}, on first need
   int64_t ncalls = 0;          // calls with record_timing
   hipStream_t last_stream = nullptr;
   std::string err;
@@ -101,7 +107,7 @@ int default_gemm_cfg(int64_t M, int64_t N, int P) {
 }
 
 struct Resolved {
-  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m, gemm_wgs;
+  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m, gemm_wgs, launch;
   uint64_t timeout_us;
 };
 
@@ -122,6 +128,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
   if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
   if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
+  if (c.launch < 0 || c.launch > 1) return fail(ctx, ENTWINE_EINVAL, "launch must be 0 or 1");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -146,6 +153,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->timeout_us = c.timeout_us ? uint64_t(c.timeout_us) : 2000000ull;
   r->group_m = c.group_m ? c.group_m : 4;
   r->gemm_wgs = c.gemm_wgs;
+  r->launch = c.launch;
   return ENTWINE_OK;
 }
 
@@ -219,7 +227,7 @@ TimingSlot* timing_slot(entwine_ctx* ctx, const Resolved& r) {
   if (!r.timing) return nullptr;
   TimingSlot* s = &ctx->ring[ctx->ncalls % kRing];
   ctx->ncalls++;
-  s->has_gemm = s->has_red = false;
+  s->has_gemm = s->has_red = s->has_stamps = false;
   return s;
 }
 
@@ -229,18 +237,19 @@ TimingSlot* timing_slot(entwine_ctx* ctx, const Resolved& r) {
 // fused path the reducer's x workgroups get the remaining CUs.
 int producer_grid(const entwine_ctx* ctx, const Resolved& r, bool fused) {
   const int nblk = int((ctx->M / r.BM) * (ctx->N / r.BN));
+  const int cus = ctx->cus > 0 ? ctx->cus : 256;
   int g = r.gemm_wgs;
   if (g <= 0) {
-    const int cus = ctx->cus > 0 ? ctx->cus : 256;
     g = fused ? cus - r.x : cus;
     g = std::max(8, (g / 8) * 8);
   }
+  // One launch holding both roles: keep every workgroup resident.
+  if (fused && r.launch == 0) g = std::max(1, std::min(g, cus - r.x));
   return std::min(g, nblk);
 }
 
-entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t lda, const void* B,
-                           int64_t ldb, void* C, int64_t ldc, bool publish, uint32_t epoch,
-                           hipStream_t s, bool fused) {
+GemmArgs gemm_args(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t lda, const void* B, int64_t ldb,
+                   void* C, int64_t ldc, bool publish, uint32_t epoch) {
   GemmArgs g;
   g.A = static_cast<const uint16_t*>(A);
   g.B = static_cast<const uint16_t*>(B);
@@ -257,6 +266,13 @@ entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, i
   g.group_m = r.group_m;
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
+  return g;
+}
+
+entwine_status launch_gemm(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t lda, const void* B,
+                           int64_t ldb, void* C, int64_t ldc, bool publish, uint32_t epoch,
+                           hipStream_t s, bool fused) {
+  const GemmArgs g = gemm_args(ctx, r, A, lda, B, ldb, C, ldc, publish, epoch);
   hipLaunchKernelGGL(gemm_kernel(r.gemm_cfg, ctx->K), dim3(producer_grid(ctx, r, fused)), dim3(256), 0, s, g);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
@@ -271,9 +287,9 @@ entwine_status launch_publish(entwine_ctx* ctx, int* flags, int64_t n, int64_t p
   return ENTWINE_OK;
 }
 
-entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* partial, int64_t ldc,
-                             const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
-                             uint32_t epoch, hipStream_t s) {
+ReduceArgs reduce_args(entwine_ctx* ctx, const Resolved& r, const void* partial, int64_t ldc,
+                       const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
+                       uint32_t epoch) {
   ReduceArgs ra;
   memset(&ra, 0, sizeof ra);
   ra.partial = static_cast<const uint16_t*>(partial);
@@ -294,7 +310,50 @@ entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* pa
   ra.epoch = epoch;
   ra.status = ctx->status;
   ra.timeout_ticks = r.timeout_us * ctx->ticks_per_us;
+  ra.publish_peers = 0;
+  ra.withhold_peer = r.withhold;
+  return ra;
+}
+
+entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* partial, int64_t ldc,
+                             const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
+                             uint32_t epoch, hipStream_t s) {
+  const ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
   hipLaunchKernelGGL(reduce_kernel(r.threads, ctx->P), dim3(r.x), dim3(r.threads), 0, s, ra);
+  HIP_OR_FAIL(ctx, hipGetLastError());
+  return ENTWINE_OK;
+}
+
+typedef void (*FusedKernel)(GemmArgs, ReduceArgs, int, int, unsigned long long*);
+template <bool TAIL>
+FusedKernel fused_kernel_t(int cfg) {
+  switch (cfg) {
+    case 0: return gemm_reduce_fused<256, 256, TAIL>;
+    case 1: return gemm_reduce_fused<256, 128, TAIL>;
+    case 2: return gemm_reduce_fused<128, 256, TAIL>;
+    default: return gemm_reduce_fused<128, 128, TAIL>;
+  }
+}
+
+// The fused path as one launch on stream s: G producer workgroups, then x
+// reducers of 256 threads that also publish the synthetic peers' flags.
+entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs& g, const void* partial,
+                            int64_t ldc, const void* const* peers, int64_t ldp, int32_t dest, void* out,
+                            int64_t ldo, uint32_t epoch, TimingSlot* ts, hipStream_t s) {
+  ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
+  ra.publish_peers = 1;
+  const int G = producer_grid(ctx, r, true);
+  const int grid = G + r.x;
+  unsigned long long* stamps = nullptr;
+  if (ts && grid <= kStampWgs) {
+    if (!ctx->stamps) HIP_OR_FAIL(ctx, hipMalloc(&ctx->stamps, size_t(kRing) * kStampWgs * 2 * sizeof(unsigned long long)));
+    stamps = ctx->stamps + size_t(ts - ctx->ring) * kStampWgs * 2;
+    ts->has_stamps = true;
+    ts->G = G;
+    ts->grid = grid;
+  }
+  FusedKernel k = ctx->K % GemmShape<128, 128>::BK ? fused_kernel_t<true>(r.gemm_cfg) : fused_kernel_t<false>(r.gemm_cfg);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, g, ra, G, ctx->P, stamps);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }
@@ -328,7 +387,7 @@ void entwine_config_default(entwine_config* cfg) {
   cfg->record_timing = 0;
   cfg->group_m = 0;
   cfg->gemm_wgs = 0;
-  cfg->reserved = 0;
+  cfg->launch = 0;
 }
 
 int32_t entwine_abi_version(void) { return ENTWINE_ABI_VERSION; }
@@ -410,6 +469,7 @@ entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
   if (ctx->status) (void)hipFree(ctx->status);
   if (ctx->scratch) (void)hipFree(ctx->scratch);
   if (ctx->zeros) (void)hipFree(ctx->zeros);
+  if (ctx->stamps) (void)hipFree(ctx->stamps);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   for (auto& s : ctx->ring) {
@@ -446,6 +506,18 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
   const bool fused = gs != rs;
   const uint32_t epoch = next_epoch(ctx);
   TimingSlot* ts = timing_slot(ctx, r);
+
+  if (fused && r.launch == 0) {
+    if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, gs));
+    const GemmArgs g = gemm_args(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch);
+    CHECK(launch_fused(ctx, r, g, partial, ldc, peers, ldp, dest, out, ldo, epoch, ts, gs));
+    if (ts) {
+      HIP_OR_FAIL(ctx, hipEventRecord(ts->red_end, gs));
+      ts->has_red = true;
+    }
+    ctx->last_stream = gs;
+    return ENTWINE_OK;
+  }
 
   if (fused) HIP_OR_FAIL(ctx, hipEventRecord(ctx->ev_fork, gs));
   if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, gs));
@@ -543,6 +615,28 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
   if (back < 0 || back >= kRing || back >= ctx->ncalls) return fail(ctx, ENTWINE_EINVAL, "no such timed call");
   TimingSlot& s = ctx->ring[(ctx->ncalls - 1 - back) % kRing];
   float g = -1.f, rd = -1.f, e = -1.f;
+  if (s.has_stamps) {
+    // Single launch: role spans from the workgroups' own timestamps, measured
+    // from the first workgroup's start; end to end from the events around it.
+    HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
+    HIP_OR_FAIL(ctx, hipEventElapsedTime(&e, s.start, s.red_end));
+    std::vector<unsigned long long> h(size_t(s.grid) * 2);
+    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * 2,
+                               h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    unsigned long long t0 = ~0ull, ge = 0, re = 0;
+    for (int b = 0; b < s.grid; ++b) {
+      t0 = std::min(t0, h[2 * b]);
+      if (b < s.G) ge = std::max(ge, h[2 * b + 1]);
+      else re = std::max(re, h[2 * b + 1]);
+    }
+    const double per_ms = double(ctx->ticks_per_us) * 1e3;
+    g = float(double(ge - t0) / per_ms);
+    rd = float(double(re - t0) / per_ms);
+    if (gemm_ms) *gemm_ms = g;
+    if (reduce_ms) *reduce_ms = rd;
+    if (e2e_ms) *e2e_ms = e;
+    return ENTWINE_OK;
+  }
   if (s.has_gemm) {
     HIP_OR_FAIL(ctx, hipEventSynchronize(s.gemm_end));
     HIP_OR_FAIL(ctx, hipEventElapsedTime(&g, s.start, s.gemm_end));

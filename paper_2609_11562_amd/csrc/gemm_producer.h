@@ -206,13 +206,15 @@ __device__ __forceinline__ void store16_wt(void* dst, u32x4_t v) {
 // issued unconditionally: past the end of the stream they re-read the last
 // slab (valid memory) into the stage that is free at that point, which no
 // real slab uses again; they are drained before the kernel ends.
+// The producer role of workgroup w of G; `smem` is GemmShape::LDS_BYTES of
+// LDS, 1 KB aligned.  Used by gemm_producer and by the single-launch fused
+// kernel, whose first G workgroups are producers.
 template <int BM, int BN, bool TAIL>
-__global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
+__device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, const int G, char* smem) {
   using S = GemmShape<BM, BN>;
   constexpr int NS = S::STAGES;
   constexpr int D = S::DMA, DH = S::DH;
   static_assert(2 * D + DH < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(1024))) char smem[S::LDS_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -225,7 +227,6 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   // loads of the next block start while the current block finishes.
   const BlockGrid grid = make_grid(a.M, a.N, a.P, BM, BN, a.group_m);
   const int nblk = grid.MB * grid.NB;
-  const int G = gridDim.x, w = blockIdx.x;
   const int mine = w < nblk ? (nblk - 1 - w) / G + 1 : 0;
   const int K = a.K;
   const int nk = (K + S::BK - 1) / S::BK;
@@ -508,6 +509,12 @@ __global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
   }
   // Loads past the end of the stream may still be writing LDS.
   if (!TAIL) wait_vm<0>();
+}
+
+template <int BM, int BN, bool TAIL>
+__global__ __launch_bounds__(256) void gemm_producer(GemmArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[GemmShape<BM, BN>::LDS_BYTES];
+  producer_body<BM, BN, TAIL>(a, blockIdx.x, gridDim.x, smem);
 }
 
 }  // namespace entwine

@@ -41,6 +41,9 @@ struct ReduceArgs {
   uint32_t epoch;
   int* status;             // {code, tile, src}
   uint64_t timeout_ticks;  // bound on one tile's waits, wall-clock ticks
+  int publish_peers;       // 1: publish the synthetic peers' flags of this
+                           // workgroup's tiles before consuming them
+  int withhold_peer;       // with publish_peers: peer left unpublished, or -1
 };
 
 typedef uint32_t r_u32x4_t __attribute__((ext_vector_type(4)));
@@ -63,20 +66,22 @@ constexpr int pow2_floor(int v) {
   return p;
 }
 
+// The reducer role of workgroup j of x (blockDim.x == THREADS); `s_abort`
+// is one int of LDS.  Used by tile_reducer and by the single-launch fused
+// kernel, whose last x workgroups are reducers.
 template <int THREADS, int NP>
-__global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
+__device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, int& s_abort) {
   constexpr int VPT = (kTile * kTile * 2 / 16) / THREADS;  // 16-byte vectors per thread
   constexpr int GMAX = 32 / NP;                             // loads in flight per lane <= 32
   constexpr int G = pow2_floor(VPT < GMAX ? VPT : GMAX);    // vectors per batch
   static_assert(VPT % G == 0, "batch must divide the per-thread vectors");
   static_assert(NP <= 64, "one polling lane per contribution");
-  __shared__ int s_abort;
 
   const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
   const int Q = tiles_per_partition(a.M, a.N, NP);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
-  const ConsumerSeq seq = consumer_seq(a.dest, NP, a.x, blockIdx.x);
+  const ConsumerSeq seq = consumer_seq(a.dest, NP, a.x, j);
   const int chunk_rows = a.M / NP;
   const int lane = threadIdx.x & 63;
   const bool poller = threadIdx.x < NP;       // lanes 0 .. NP-1 of wave 0
@@ -113,6 +118,15 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
     if (lane == 0) acquire_fence();
     return true;
   };
+
+  // Synthetic peers: their producers have nothing left to compute on this
+  // GPU, so the flags of this workgroup's tiles are published up front, by
+  // the lanes that poll them.
+  if (a.publish_peers && threadIdx.x >= 1 && threadIdx.x < NP && threadIdx.x - 1 != a.withhold_peer) {
+    for (int tt = seq.first; tt < Q; tt += seq.stride)
+      publish_relaxed(const_cast<int*>(a.peer_flags) + static_cast<int64_t>(threadIdx.x - 1) * ntiles + global_tile(tt),
+                      a.epoch);
+  }
 
   int t = seq.first;
   if (t >= Q) return;
@@ -181,6 +195,12 @@ __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
     __syncthreads();
     if (s_abort) return;
   }
+}
+
+template <int THREADS, int NP>
+__global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
+  __shared__ int s_abort;
+  reducer_body<THREADS, NP>(a, blockIdx.x, s_abort);
 }
 
 // Publishes the synthetic peers' flags for this call (they stand in for the

@@ -71,6 +71,8 @@ def test_validate_config(lib):
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_threads=64)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(withhold_peer=1)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(withhold_peer=0)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=1)) == E.OK
 
 
 SHAPES = [(512, 1024, 2, 256, 256), (4096, 4096, 8, 256, 256), (4096, 4096, 8, 128, 128),

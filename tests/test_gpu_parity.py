@@ -133,7 +133,9 @@ def test_results_independent_of_order_budget_threads_and_mode():
                    [dict(gemm_wgs=8), dict(gemm_cfg=1, gemm_wgs=24), dict(gemm_cfg=2, gemm_wgs=16),
                     dict(gemm_cfg=3, gemm_wgs=40)] + \
                    [dict(reduce_wgs=x) for x in (4, 8, 32, 64)] + \
-                   [dict(reduce_threads=b) for b in (128, 512)]
+                   [dict(reduce_threads=b) for b in (128, 512)] + \
+                   [dict(launch=1), dict(launch=1, reduce_threads=512, reduce_wgs=8),
+                    dict(launch=1, gemm_cfg=3, reduce_threads=1024)]
         for kw in variants:
             o = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(**kw)))
             assert np.array_equal(o, base), kw
@@ -171,13 +173,14 @@ def test_reducer_is_exact_on_given_partial():
 def test_withheld_peer_times_out_then_recovers(tiny):
     w, prob, ctx, (A, B, peers) = tiny
     print("[timeout]", flush=True)
-    cfg = E.Config.make(withhold_peer=0, timeout_us=20000, reduce_wgs=2)
-    ctx.gemm_rs(A, B, peers, 1, cfg=cfg, reduce_stream=torch.cuda.Stream())
-    st, tile, src = ctx.query_status()
-    assert st == E.ETIMEOUT and src == 0 and 0 <= tile < (w.M // 128) * (w.N // 128)
-    o = run(ctx, A, B, peers, 1)
-    torch.cuda.synchronize()
-    check_rows(prob, host_bits(o), out_global_rows(w.M, w.P, 1))
+    for launch in (0, 1):
+        cfg = E.Config.make(withhold_peer=0, timeout_us=20000, reduce_wgs=2, launch=launch)
+        ctx.gemm_rs(A, B, peers, 1, cfg=cfg, reduce_stream=torch.cuda.Stream())
+        st, tile, src = ctx.query_status()
+        assert st == E.ETIMEOUT and src == 0 and 0 <= tile < (w.M // 128) * (w.N // 128), launch
+        o = run(ctx, A, B, peers, 1)
+        torch.cuda.synchronize()
+        check_rows(prob, host_bits(o), out_global_rows(w.M, w.P, 1))
 
 
 def test_poisoned_buffers_never_leak_across_repeated_calls():
@@ -199,7 +202,7 @@ def test_poisoned_buffers_never_leak_across_repeated_calls():
             partial.fill_(nan)
             out.fill_(nan)
             ctx.gemm_rs(A, B, peers, 5, out=out, partial=partial, reduce_stream=rs,
-                        cfg=E.Config.make(reduce_wgs=8 + i))
+                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 2))
             got = host_bits(out)
             if i < 2:
                 check_rows(probs[i], got, out_global_rows(M, P, 5))
