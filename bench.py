@@ -50,6 +50,40 @@ def parse():
     return ap.parse_args()
 
 
+def kernel_sources_hash(root: str) -> str:
+    """First 16 hex digits of the SHA-256 over the HIP sources and the ABI
+    header, in a fixed order; identifies the kernels a counter run measured."""
+    import glob
+    import hashlib
+    pkg = os.path.join(root, "paper_2609_11562_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(pkg, "*.h"))) + sorted(glob.glob(os.path.join(pkg, "*.hip"))) + \
+        [os.path.join(root, "include", "entwine.h")]
+    h = hashlib.sha256()
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(root: str, workload: str, kernel: str, cfg_now: dict):
+    """HBM bytes per launch of the dominant kernel from the recorded counter
+    runs (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by the same
+    counter's reading on a device copy of known size), or None when none was
+    taken for this workload, kernel, configuration and kernel sources."""
+    path = os.path.join(root, "paper_2609_11562_amd", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        e = json.load(f).get(workload)
+    if not e or not e["kernel"].startswith(kernel) or e["sources_sha256_16"] != kernel_sources_hash(root):
+        return None
+    if any(cfg_now.get(k) != v for k, v in e["config"].items()):
+        return None
+    rd = e["fetch_kib"] * 1024 * e["fetch_scale"]
+    wr = e["write_kib"] * 1024 * e["write_scale"]
+    return {"bytes": round(rd + wr), "read": round(rd), "written": round(wr), "source": e["profile"]}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -148,6 +182,12 @@ def main():
     mean_k = statistics.fmean(e_ms) if single and e_ms else mean_g
     kernel = "gemm_reduce_fused" if single else "gemm_producer"
     achieved = flops / (mean_k * 1e-3) / 1e12 if mean_k else None
+    root = os.path.dirname(os.path.abspath(__file__))
+    cfg_now = {"dest": dest_mode, "gemm_cfg": cfg.gemm_cfg, "reduce_wgs": cfg.reduce_wgs, "group_m": cfg.group_m,
+               "launch": cfg.launch}
+    traffic = measured_traffic(root, w.name, kernel, cfg_now) if main_mode == "fused" else None
+    rows_out = M if all_chunks else M // P
+    algo_bytes = 2.0 * (M * K + K * N + M * N) + 2.0 * rows_out * N * (P + 1)
 
     legs = {}
     if not args.no_legs and args.only is None:
@@ -212,7 +252,9 @@ def main():
                      "achieved": round(achieved, 2) if achieved else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
-                     "traffic": None,
+                     "traffic": traffic["bytes"] if traffic else None,
+                     "traffic_detail": traffic,
+                     "algorithmic_bytes": round(algo_bytes),
                      "kernel_mean_ms": round(mean_k, 5) if mean_k else None,
                      "producer_span_ms": round(mean_g, 5) if mean_g else None,
                      "producer_tflops": round(flops / (mean_g * 1e-3) / 1e12, 2) if mean_g else None},
