@@ -78,7 +78,10 @@ typedef struct {
   int32_t reduce_wgs;     /* x: reducer grid size, the communication budget
                              (Section 3.2); 0 = default; capped at the tile
                              count and at CUs - 1.  With DEST_ALL it is
-                             rounded up to a multiple of P. */
+                             rounded up to a multiple of P.  With launch 0,
+                             producers that finish their blocks also take
+                             tiles, and -1 asks for no dedicated reducers
+                             at all (all CUs produce, then reduce). */
   int32_t reduce_threads; /* b: threads per reducer workgroup, 128/256/512/1024
                              (0 = default = 1024) */
   int32_t timeout_us;     /* bound on one reducer wait, microseconds
@@ -99,7 +102,11 @@ typedef struct {
                              threads (reduce_threads then does not apply;
                              G is capped so that all are resident);
                              1 = two kernels on the two streams (Section
-                             4.3's form), with b threads per reducer */
+                             4.3's form), with b threads per reducer;
+                             2 = shared pool (Section 5.3.2): the producer
+                             on every CU and x small reducer workgroups of
+                             256 threads beside it (default x: one per CU);
+                             1 and 0 partition the CUs instead */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */

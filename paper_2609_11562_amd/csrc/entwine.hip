@@ -61,7 +61,8 @@ struct entwine_ctx {
   uint64_t ticks_per_us = 100;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   TimingSlot ring[kRing];
-  unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, end}, on first need
+  unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, producer end, end}, on first need
+  unsigned int* task_ctr = nullptr;       // single launch: {next task, finished workgroups}, zero between calls
   int64_t ncalls = 0;          // calls with record_timing
   hipStream_t last_stream = nullptr;
   std::string err;
@@ -107,7 +108,10 @@ int default_gemm_cfg(int64_t M, int64_t N, int P) {
 }
 
 struct Resolved {
-  int order, gemm_cfg, BM, BN, x, threads, withhold, timing, group_m, gemm_wgs, launch;
+  // x: dedicated reducer workgroups of the fused launch (0 with reduce_wgs
+  // -1); x_alone: grid of the standalone reducer kernel (reduce_only, the
+  // sequential form and the two-stream forms), never 0.
+  int order, gemm_cfg, BM, BN, x, x_alone, threads, withhold, timing, group_m, gemm_wgs, launch;
   uint64_t timeout_us;
 };
 
@@ -123,12 +127,13 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.reduce_threads != 0 && c.reduce_threads != 128 && c.reduce_threads != 256 && c.reduce_threads != 512 &&
       c.reduce_threads != 1024)
     return fail(ctx, ENTWINE_EINVAL, "reduce_threads must be 128, 256, 512 or 1024");
-  if (c.reduce_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "reduce_wgs must be >= 0");
+  if (c.reduce_wgs < -1 || (c.reduce_wgs == -1 && c.launch != 0))
+    return fail(ctx, ENTWINE_EINVAL, "reduce_wgs must be >= 0 (or -1 with launch 0)");
   if (c.timeout_us < 0) return fail(ctx, ENTWINE_EINVAL, "timeout_us must be >= 0");
   if (c.withhold_peer < -1 || c.withhold_peer > P - 2) return fail(ctx, ENTWINE_EINVAL, "withhold_peer outside [-1, P-2]");
   if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
   if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
-  if (c.launch < 0 || c.launch > 1) return fail(ctx, ENTWINE_EINVAL, "launch must be 0 or 1");
+  if (c.launch < 0 || c.launch > 2) return fail(ctx, ENTWINE_EINVAL, "launch must be 0, 1 or 2");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -137,7 +142,9 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
     return fail(ctx, ENTWINE_EUNSUPPORTED, "block %dx%d does not divide the %lldx%lld chunk", r->BM, r->BN,
                 (long long)(M / P), (long long)N);
   const int Q = tiles_per_partition(int(M), int(N), P);
-  int x = c.reduce_wgs > 0 ? c.reduce_wgs : 16;
+  // Default budget: 16 dedicated reducer CUs; in the shared pool one reducer
+  // workgroup per CU.
+  int x = c.reduce_wgs > 0 ? c.reduce_wgs : (c.launch == 2 ? std::max(16, cus) : 16);
   const int cap_cus = std::max(1, (cus > 1 ? cus - 1 : 255));
   if (dest == ENTWINE_DEST_ALL) {
     x = std::min(x, Q * P);
@@ -146,7 +153,8 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   } else {
     x = std::min(std::min(x, Q), cap_cus);
   }
-  r->x = std::max(x, 1);
+  r->x_alone = std::max(x, 1);
+  r->x = c.reduce_wgs == -1 ? 0 : r->x_alone;
   r->threads = c.reduce_threads ? c.reduce_threads : 1024;
   r->withhold = c.withhold_peer;
   r->timing = c.record_timing;
@@ -200,6 +208,19 @@ ReduceKernel reduce_kernel_p(int P) {
     default: return tile_reducer<T, 8>;
   }
 }
+ReduceKernel shared_reduce_kernel(int P) {
+  switch (P) {
+    case 1: return tile_reducer_shared<1>;
+    case 2: return tile_reducer_shared<2>;
+    case 3: return tile_reducer_shared<3>;
+    case 4: return tile_reducer_shared<4>;
+    case 5: return tile_reducer_shared<5>;
+    case 6: return tile_reducer_shared<6>;
+    case 7: return tile_reducer_shared<7>;
+    default: return tile_reducer_shared<8>;
+  }
+}
+
 ReduceKernel reduce_kernel(int threads, int P) {
   if (threads == 128) return reduce_kernel_p<128>(P);
   if (threads == 512) return reduce_kernel_p<512>(P);
@@ -301,7 +322,7 @@ ReduceArgs reduce_args(entwine_ctx* ctx, const Resolved& r, const void* partial,
   ra.M = int(ctx->M);
   ra.N = int(ctx->N);
   ra.dest = dest;
-  ra.x = r.x;
+  ra.x = r.x_alone;
   ra.BM = r.BM;
   ra.BN = r.BN;
   ra.group_m = r.group_m;
@@ -319,7 +340,24 @@ entwine_status launch_reduce(entwine_ctx* ctx, const Resolved& r, const void* pa
                              const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
                              uint32_t epoch, hipStream_t s) {
   const ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
-  hipLaunchKernelGGL(reduce_kernel(r.threads, ctx->P), dim3(r.x), dim3(r.threads), 0, s, ra);
+  hipLaunchKernelGGL(reduce_kernel(r.threads, ctx->P), dim3(r.x_alone), dim3(r.threads), 0, s, ra);
+  HIP_OR_FAIL(ctx, hipGetLastError());
+  return ENTWINE_OK;
+}
+
+// Shared pool: reducers of 256 threads beside the producers on the same CUs,
+// publishing the synthetic peers' flags themselves.
+entwine_status launch_reduce_shared(entwine_ctx* ctx, const Resolved& r, const void* partial, int64_t ldc,
+                                    const void* const* peers, int64_t ldp, int32_t dest, void* out, int64_t ldo,
+                                    uint32_t epoch, hipStream_t s) {
+  // The shared-pool reducer addresses every matrix with 32-bit byte offsets.
+  const int64_t rows = ctx->M;
+  for (int64_t ld : {ldc, ldp, ldo})
+    if ((rows * ld + ctx->N) * 2 > (int64_t(1) << 32))
+      return fail(ctx, ENTWINE_EUNSUPPORTED, "launch=2 needs matrices under 4 GiB (ld %lld)", (long long)ld);
+  ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
+  ra.publish_peers = 1;
+  hipLaunchKernelGGL(shared_reduce_kernel(ctx->P), dim3(r.x_alone), dim3(256), 0, s, ra);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }
@@ -341,13 +379,14 @@ entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs&
                             int64_t ldc, const void* const* peers, int64_t ldp, int32_t dest, void* out,
                             int64_t ldo, uint32_t epoch, TimingSlot* ts, hipStream_t s) {
   ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
-  ra.publish_peers = 1;
+  ra.task_ctr = ctx->task_ctr;
+  ra.ntasks = tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
   const int G = producer_grid(ctx, r, true);
   const int grid = G + r.x;
   unsigned long long* stamps = nullptr;
   if (ts && grid <= kStampWgs) {
-    if (!ctx->stamps) HIP_OR_FAIL(ctx, hipMalloc(&ctx->stamps, size_t(kRing) * kStampWgs * 2 * sizeof(unsigned long long)));
-    stamps = ctx->stamps + size_t(ts - ctx->ring) * kStampWgs * 2;
+    if (!ctx->stamps) HIP_OR_FAIL(ctx, hipMalloc(&ctx->stamps, size_t(kRing) * kStampWgs * 3 * sizeof(unsigned long long)));
+    stamps = ctx->stamps + size_t(ts - ctx->ring) * kStampWgs * 3;
     ts->has_stamps = true;
     ts->G = G;
     ts->grid = grid;
@@ -442,11 +481,13 @@ entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, 
   const size_t fbytes = size_t(c->ntiles) * sizeof(int);
   if (hipMalloc(&c->flags, fbytes) != hipSuccess ||
       hipMalloc(&c->peer_flags, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
-      hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess || hipMalloc(&c->zeros, 256) != hipSuccess)
+      hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess || hipMalloc(&c->zeros, 256) != hipSuccess ||
+      hipMalloc(&c->task_ctr, 2 * sizeof(unsigned int)) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_ENOMEM, "flag allocation failed"));
   if (hipMemset(c->flags, 0, fbytes) != hipSuccess ||
       hipMemset(c->peer_flags, 0, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
-      hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess || hipMemset(c->zeros, 0, 256) != hipSuccess)
+      hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess || hipMemset(c->zeros, 0, 256) != hipSuccess ||
+      hipMemset(c->task_ctr, 0, 2 * sizeof(unsigned int)) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_EHIP, "flag initialisation failed"));
   if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
@@ -470,6 +511,7 @@ entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
   if (ctx->scratch) (void)hipFree(ctx->scratch);
   if (ctx->zeros) (void)hipFree(ctx->zeros);
   if (ctx->stamps) (void)hipFree(ctx->stamps);
+  if (ctx->task_ctr) (void)hipFree(ctx->task_ctr);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   for (auto& s : ctx->ring) {
@@ -519,16 +561,21 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
     return ENTWINE_OK;
   }
 
+  const bool shared = fused && r.launch == 2;
   if (fused) HIP_OR_FAIL(ctx, hipEventRecord(ctx->ev_fork, gs));
   if (ts) HIP_OR_FAIL(ctx, hipEventRecord(ts->start, gs));
-  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, gs, fused));
+  CHECK(launch_gemm(ctx, r, A, lda, B, ldb, partial, ldc, true, epoch, gs, fused && !shared));
   if (ts) {
     HIP_OR_FAIL(ctx, hipEventRecord(ts->gemm_end, gs));
     ts->has_gemm = true;
   }
   if (fused) HIP_OR_FAIL(ctx, hipStreamWaitEvent(rs, ctx->ev_fork, 0));
-  CHECK(launch_publish(ctx, ctx->peer_flags, ctx->ntiles * (ctx->P - 1), ctx->ntiles, r.withhold, epoch, rs));
-  CHECK(launch_reduce(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch, rs));
+  if (shared) {
+    CHECK(launch_reduce_shared(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch, rs));
+  } else {
+    CHECK(launch_publish(ctx, ctx->peer_flags, ctx->ntiles * (ctx->P - 1), ctx->ntiles, r.withhold, epoch, rs));
+    CHECK(launch_reduce(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch, rs));
+  }
   if (ts) {
     HIP_OR_FAIL(ctx, hipEventRecord(ts->red_end, rs));
     ts->has_red = true;
@@ -620,14 +667,14 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
     // from the first workgroup's start; end to end from the events around it.
     HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
     HIP_OR_FAIL(ctx, hipEventElapsedTime(&e, s.start, s.red_end));
-    std::vector<unsigned long long> h(size_t(s.grid) * 2);
-    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * 2,
+    std::vector<unsigned long long> h(size_t(s.grid) * 3);
+    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * 3,
                                h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
     unsigned long long t0 = ~0ull, ge = 0, re = 0;
     for (int b = 0; b < s.grid; ++b) {
-      t0 = std::min(t0, h[2 * b]);
-      if (b < s.G) ge = std::max(ge, h[2 * b + 1]);
-      else re = std::max(re, h[2 * b + 1]);
+      t0 = std::min(t0, h[3 * b]);
+      if (b < s.G) ge = std::max(ge, h[3 * b + 1]);
+      re = std::max(re, h[3 * b + 2]);
     }
     const double per_ms = double(ctx->ticks_per_us) * 1e3;
     g = float(double(ge - t0) / per_ms);

@@ -5,11 +5,15 @@
 // Both roles are persistent and one workgroup fits a CU (the producer's LDS
 // stages fill it), so with G + x no larger than the CU count every workgroup
 // is resident at once and the reducers run on their own x CUs, the paper's
-// partition of the device between computation and communication.  Only
-// reducers ever wait, and only for producers, so progress never depends on
-// residency order.  One launch replaces the two kernels, the synthetic
-// peer-flag kernel and the two cross-stream event waits of the two-stream
-// form, each of which costs microseconds of queue synchronisation per call.
+// partition of the device between computation and communication.  Tiles are
+// handed out in consumer order from a device counter, and a producer that has
+// finished its blocks becomes a reducer too: at the end of the GEMM the
+// remaining tiles are reduced by the whole device instead of by x CUs, and a
+// block count that is not a multiple of G leaves no CU idle.  Only reducers
+// ever wait, and only for producers, so progress never depends on residency
+// order.  One launch replaces the two kernels, the synthetic peer-flag kernel
+// and the two cross-stream event waits of the two-stream form, each of which
+// costs microseconds of queue synchronisation per call.
 #pragma once
 
 #include "gemm_producer.h"
@@ -17,34 +21,34 @@
 
 namespace entwine {
 
-// stamps: null, or 2 per workgroup {start, end} in wall-clock ticks.
+// stamps: null, or 3 per workgroup {start, producer end, end} in wall-clock
+// ticks (producer end = start for workgroups without producer work).
 template <int BM, int BN, bool TAIL>
 __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs r, int G, int np,
                                                           unsigned long long* stamps) {
   __shared__ __attribute__((aligned(1024))) char smem[GemmShape<BM, BN>::LDS_BYTES];
   const unsigned long long t0 = stamps ? wall_clock64() : 0;
   const int b = blockIdx.x;
-  if (b < G) {
-    producer_body<BM, BN, TAIL>(g, b, G, smem);
-  } else {
-    int& s_abort = *reinterpret_cast<int*>(smem);
-    const int j = b - G;
-    switch (np) {
-      case 1: reducer_body<256, 1>(r, j, s_abort); break;
-      case 2: reducer_body<256, 2>(r, j, s_abort); break;
-      case 3: reducer_body<256, 3>(r, j, s_abort); break;
-      case 4: reducer_body<256, 4>(r, j, s_abort); break;
-      case 5: reducer_body<256, 5>(r, j, s_abort); break;
-      case 6: reducer_body<256, 6>(r, j, s_abort); break;
-      case 7: reducer_body<256, 7>(r, j, s_abort); break;
-      default: reducer_body<256, 8>(r, j, s_abort); break;
-    }
+  publish_peer_slice(r, np, b, gridDim.x);
+  if (b < G) producer_body<BM, BN, TAIL>(g, b, G, smem);
+  const unsigned long long t1 = stamps ? wall_clock64() : 0;
+  int* s = reinterpret_cast<int*>(smem);
+  switch (np) {
+    case 1: reducer_dynamic<256, 1>(r, s); break;
+    case 2: reducer_dynamic<256, 2>(r, s); break;
+    case 3: reducer_dynamic<256, 3>(r, s); break;
+    case 4: reducer_dynamic<256, 4>(r, s); break;
+    case 5: reducer_dynamic<256, 5>(r, s); break;
+    case 6: reducer_dynamic<256, 6>(r, s); break;
+    case 7: reducer_dynamic<256, 7>(r, s); break;
+    default: reducer_dynamic<256, 8>(r, s); break;
   }
   if (stamps) {
     __syncthreads();
     if (threadIdx.x == 0) {
-      stamps[2 * b] = t0;
-      stamps[2 * b + 1] = wall_clock64();
+      stamps[3 * b] = t0;
+      stamps[3 * b + 1] = b < G ? t1 : t0;
+      stamps[3 * b + 2] = wall_clock64();
     }
   }
 }

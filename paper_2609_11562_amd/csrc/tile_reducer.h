@@ -44,6 +44,8 @@ struct ReduceArgs {
   int publish_peers;       // 1: publish the synthetic peers' flags of this
                            // workgroup's tiles before consuming them
   int withhold_peer;       // with publish_peers: peer left unpublished, or -1
+  unsigned int* task_ctr;  // dynamic tasks: {next task, finished workgroups}
+  int ntasks;              // dynamic tasks: tiles this call reduces
 };
 
 typedef uint32_t r_u32x4_t __attribute__((ext_vector_type(4)));
@@ -60,29 +62,111 @@ __device__ __forceinline__ r_u32x4_t ld_stream(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const r_u32x4_t*>(p));
 }
 
+__device__ __forceinline__ r_u32x4_t ld_stream_at(const uint16_t* base, uint32_t byte_off) {
+  return __builtin_nontemporal_load(reinterpret_cast<const r_u32x4_t*>(reinterpret_cast<const char*>(base) + byte_off));
+}
+
 constexpr int pow2_floor(int v) {
   int p = 1;
   while (p * 2 <= v) p *= 2;
   return p;
 }
 
-// The reducer role of workgroup j of x (blockDim.x == THREADS); `s_abort`
-// is one int of LDS.  Used by tile_reducer and by the single-launch fused
-// kernel, whose last x workgroups are reducers.
-template <int THREADS, int NP>
-__device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, int& s_abort) {
+// Flag polled by lane `lane` of a waiting wave for global tile gt: lane 0
+// the local flag, lane q+1 peer q's.
+__device__ __forceinline__ const int* flag_of_lane(const ReduceArgs& a, int lane, int ntiles, int gt) {
+  return lane == 0 ? a.flags + gt : a.peer_flags + static_cast<int64_t>(lane - 1) * ntiles + gt;
+}
+
+// One wave (lanes 0 .. np-1 poll): wait until every flag of tile gt equals
+// the epoch (`seen` holds a first poll already made by this lane), sleeping
+// `nap` units between polls.  Returns false, after recording the timeout in
+// the status word, if the deadline passes first.
+__device__ __forceinline__ bool wave_await_tile(const ReduceArgs& a, int gt, int ntiles, int np, int seen, int nap) {
+  const int lane = threadIdx.x & 63;
+  const bool poller = lane < np;
+  const int epoch = static_cast<int>(a.epoch);
+  bool ready = !poller || seen == epoch;
+  const uint64_t deadline = wall_clock64() + a.timeout_ticks;
+  while (__ballot(!ready) != 0) {
+    if (wall_clock64() > deadline) {
+      const int first = __builtin_ctzll(__ballot(!ready));
+      if (lane == 0 && atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
+        atomicExch(a.status + 1, gt);
+        atomicExch(a.status + 2, first == 0 ? -1 : first - 1);   // -1 local, q peer q
+      }
+      return false;
+    }
+    if (nap > 1) __builtin_amdgcn_s_sleep(8);
+    else __builtin_amdgcn_s_sleep(1);
+    if (!ready) ready = poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) == epoch;
+  }
+  return true;
+}
+
+// Reduces global tile gt with THREADS threads: every element starts from the
+// local contribution, the peers are added in rank order in fp32, the result
+// is rounded to bf16 and stored once.  G vectors of every contribution are
+// loaded per lane before any is consumed; `after_first_loads` runs right
+// after the first batch of loads is issued (used to overlap a flag poll).
+template <int THREADS, int NP, typename Hook>
+__device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int tiles_n, Hook after_first_loads) {
   constexpr int VPT = (kTile * kTile * 2 / 16) / THREADS;  // 16-byte vectors per thread
   constexpr int GMAX = 32 / NP;                             // loads in flight per lane <= 32
   constexpr int G = pow2_floor(VPT < GMAX ? VPT : GMAX);    // vectors per batch
   static_assert(VPT % G == 0, "batch must divide the per-thread vectors");
-  static_assert(NP <= 64, "one polling lane per contribution");
+  const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile;
+  const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
+  const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * (a.M / NP) : grow0;
+#pragma unroll
+  for (int v0 = 0; v0 < VPT; v0 += G) {
+    r_u32x4_t lv[G];
+    r_u32x4_t pv[NP > 1 ? NP - 1 : 1][G];
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      const int v = threadIdx.x + THREADS * (v0 + gi);
+      const int64_t r = v >> 4, cc = (v & 15) * 8;
+      lv[gi] = ld_stream(a.partial + (grow0 + r) * a.ldc + gcol0 + cc);
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q) pv[q][gi] = ld_stream(a.peers[q] + (grow0 + r) * a.ldp + gcol0 + cc);
+    }
+    if (v0 == 0) after_first_loads();
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = __builtin_bit_cast(float, lv[gi][e] << 16);
+        acc[2 * e + 1] = __builtin_bit_cast(float, lv[gi][e] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __builtin_bit_cast(float, pv[q][gi][e] << 16);
+          acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][gi][e] & 0xffff0000u);
+        }
+      r_u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+      const int v = threadIdx.x + THREADS * (v0 + gi);
+      const int64_t r = v >> 4, cc = (v & 15) * 8;
+      __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc));
+    }
+  }
+}
 
+// The reducer role of workgroup j of x (blockDim.x == THREADS), with the
+// paper's static task order (tiles j, j+x, ... of its partition); `s_abort`
+// is one int of LDS.  Used by tile_reducer.
+template <int THREADS, int NP>
+__device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, int& s_abort) {
+  static_assert(NP <= 64, "one polling lane per contribution");
   const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
   const int Q = tiles_per_partition(a.M, a.N, NP);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
   const ConsumerSeq seq = consumer_seq(a.dest, NP, a.x, j);
-  const int chunk_rows = a.M / NP;
   const int lane = threadIdx.x & 63;
   const bool poller = threadIdx.x < NP;       // lanes 0 .. NP-1 of wave 0
   const int epoch = static_cast<int>(a.epoch);
@@ -91,32 +175,6 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
     int tr, tc;
     tile_of_number(seq.part, t, grid, &tr, &tc);
     return tr * tiles_n + tc;
-  };
-  // Flag polled by this lane: lane 0 the local flag, lane q+1 peer q's.
-  auto flag_of = [&](int gt) {
-    return lane == 0 ? a.flags + gt : a.peer_flags + static_cast<int64_t>(lane - 1) * ntiles + gt;
-  };
-  // Wave 0: wait until every flag of tile gt is ready (`seen` holds a first
-  // poll already made), then acquire; returns false, after recording the
-  // timeout, if the deadline passes first.  Called by wave 0 only.
-  auto await_tile = [&](int gt, int seen) {
-    bool ready = !poller || seen == epoch;
-    const uint64_t deadline = wall_clock64() + a.timeout_ticks;
-    while (__ballot(!ready) != 0) {
-      if (wall_clock64() > deadline) {
-        const uint64_t missing = __ballot(!ready);
-        const int first = __builtin_ctzll(missing);
-        if (lane == 0 && atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
-          atomicExch(a.status + 1, gt);
-          atomicExch(a.status + 2, first == 0 ? -1 : first - 1);   // -1 local, q peer q
-        }
-        return false;
-      }
-      __builtin_amdgcn_s_sleep(1);
-      if (!ready) ready = poll_relaxed(flag_of(gt)) == epoch;
-    }
-    if (lane == 0) acquire_fence();
-    return true;
   };
 
   // Synthetic peers: their producers have nothing left to compute on this
@@ -131,69 +189,95 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
   int t = seq.first;
   if (t >= Q) return;
   int gt = global_tile(t);
-  if (threadIdx.x < 64) {
-    const int seen = poller ? poll_relaxed(flag_of(gt)) : epoch;
-    const bool ok = await_tile(gt, seen);
-    if (lane == 0) s_abort = !ok;
-  }
-  __syncthreads();
-  if (s_abort) return;
-
+  int seen = poller ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : epoch;
   while (true) {
-    const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile;
-    const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
-    const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * chunk_rows : grow0;
-    const int tn = t + seq.stride;
-    const int gtn = tn < Q ? global_tile(tn) : 0;
-    int seen = epoch;
-
-#pragma unroll
-    for (int v0 = 0; v0 < VPT; v0 += G) {
-      r_u32x4_t lv[G];
-      r_u32x4_t pv[NP > 1 ? NP - 1 : 1][G];
-#pragma unroll
-      for (int gi = 0; gi < G; ++gi) {
-        const int v = threadIdx.x + THREADS * (v0 + gi);
-        const int64_t r = v >> 4, cc = (v & 15) * 8;
-        lv[gi] = ld_stream(a.partial + (grow0 + r) * a.ldc + gcol0 + cc);
-#pragma unroll
-        for (int q = 0; q < NP - 1; ++q) pv[q][gi] = ld_stream(a.peers[q] + (grow0 + r) * a.ldp + gcol0 + cc);
-      }
-      // First poll of the next tile's flags, behind the first batch's loads.
-      if (v0 == 0 && poller && tn < Q) seen = poll_relaxed(flag_of(gtn));
-#pragma unroll
-      for (int gi = 0; gi < G; ++gi) {
-        float acc[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] = __builtin_bit_cast(float, lv[gi][e] << 16);
-          acc[2 * e + 1] = __builtin_bit_cast(float, lv[gi][e] & 0xffff0000u);
-        }
-#pragma unroll
-        for (int q = 0; q < NP - 1; ++q)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc[2 * e] += __builtin_bit_cast(float, pv[q][gi][e] << 16);
-            acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][gi][e] & 0xffff0000u);
-          }
-        r_u32x4_t o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
-        const int v = threadIdx.x + THREADS * (v0 + gi);
-        const int64_t r = v >> 4, cc = (v & 15) * 8;
-        __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc));
-      }
-    }
-    if (tn >= Q) break;
-    t = tn;
-    gt = gtn;
-    __syncthreads();   // s_abort is rewritten below
     if (threadIdx.x < 64) {
-      const bool ok = await_tile(gt, seen);
+      const bool ok = wave_await_tile(a, gt, ntiles, NP, seen, 1);
+      if (ok && lane == 0) acquire_fence();
       if (lane == 0) s_abort = !ok;
     }
     __syncthreads();
     if (s_abort) return;
+    const int tn = t + seq.stride;
+    const int gtn = tn < Q ? global_tile(tn) : 0;
+    seen = epoch;
+    // The first poll of the next tile's flags rides behind this tile's loads.
+    reduce_tile<THREADS, NP>(a, gt, tiles_n, [&] {
+      if (poller && tn < Q) seen = poll_relaxed(flag_of_lane(a, lane, ntiles, gtn));
+    });
+    if (tn >= Q) break;
+    t = tn;
+    gt = gtn;
+    __syncthreads();   // s_abort is rewritten next
+  }
+}
+
+// Publishes, as part of one launch, the synthetic peers' flags of every tile
+// the call reduces (`ntasks` tiles in consumer order, see task_tile), split
+// over all nb workgroups; peer `withhold_peer` stays unpublished.
+__device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, int b, int nb) {
+  const BlockGrid grid = make_grid(a.M, a.N, np, a.BM, a.BN, a.group_m);
+  const int tiles_n = a.N / kTile;
+  const int ntiles = (a.M / kTile) * tiles_n;
+  const int64_t n = static_cast<int64_t>(np - 1) * a.ntasks;
+  for (int64_t i = static_cast<int64_t>(b) * blockDim.x + threadIdx.x; i < n;
+       i += static_cast<int64_t>(nb) * blockDim.x) {
+    const int q = static_cast<int>(i / a.ntasks), task = static_cast<int>(i % a.ntasks);
+    if (q == a.withhold_peer) continue;
+    const int part = a.dest >= 0 ? a.dest : task % np;
+    const int idx = a.dest >= 0 ? task : task / np;
+    int tr, tc;
+    tile_of_number(part, idx, grid, &tr, &tc);
+    publish_relaxed(const_cast<int*>(a.peer_flags) + static_cast<int64_t>(q) * ntiles + tr * tiles_n + tc, a.epoch);
+  }
+}
+
+// The reducer role with dynamic tasks: workgroups take tiles from a device
+// counter in consumer order (task t is tile t of the destination's
+// partition; with every destination, tile t / P of partition t % P, which
+// interleaves the partitions as Equation 1 does), so the dedicated reducers
+// and every producer that has finished its blocks share the remaining tiles.
+// Each workgroup ends with one failed take; the last workgroup of the grid to
+// finish returns both counters to zero, ready for the next call.  After a
+// timeout waits are skipped (the call's output is then undefined) but the
+// task accounting stays exact.  s: two ints of LDS.
+template <int THREADS, int NP>
+__device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
+  const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
+  const int tiles_n = a.N / kTile;
+  const int ntiles = (a.M / kTile) * tiles_n;
+  const int lane = threadIdx.x & 63;
+  auto task_tile = [&](int task) {
+    const int part = a.dest >= 0 ? a.dest : task % NP;
+    const int idx = a.dest >= 0 ? task : task / NP;
+    int tr, tc;
+    tile_of_number(part, idx, grid, &tr, &tc);
+    return tr * tiles_n + tc;
+  };
+  __syncthreads();   // producer waves are done with the LDS
+  if (threadIdx.x == 0) s[0] = static_cast<int>(atomicAdd(a.task_ctr, 1u));
+  __syncthreads();
+  int task = s[0];
+  bool timed_out = false;   // wave 0
+  while (task < a.ntasks) {
+    const int gt = task_tile(task);
+    if (threadIdx.x < 64) {
+      if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
+      if (!timed_out) {
+        const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
+        timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
+      }
+      if (lane == 0) acquire_fence();
+    }
+    __syncthreads();
+    const int next = s[1];
+    reduce_tile<THREADS, NP>(a, gt, tiles_n, [] {});
+    __syncthreads();   // s[1] is rewritten next
+    task = next;
+  }
+  if (threadIdx.x == 0 && atomicAdd(a.task_ctr + 1, 1u) == gridDim.x - 1) {
+    atomicExch(a.task_ctr, 0u);
+    atomicExch(a.task_ctr + 1, 0u);
   }
 }
 
@@ -201,6 +285,111 @@ template <int THREADS, int NP>
 __global__ __launch_bounds__(THREADS) void tile_reducer(ReduceArgs a) {
   __shared__ int s_abort;
   reducer_body<THREADS, NP>(a, blockIdx.x, s_abort);
+}
+
+// The shared-pool form (paper Section 5.3.2, shared versus partitioned
+// resources): reducer workgroups small enough to sit beside a producer
+// workgroup on the same CU, so the reduction is spread over every CU instead
+// of taking CUs away from the GEMM.  A producer wave holds at most 448 of the
+// 512 registers per lane of its SIMD and the producer fills the LDS, so a
+// reducer wave here uses at most 64 registers and no LDS.
+//   * Only wave 0 polls a tile's flags (lanes 0 .. P-1), backing off between
+//     polls, so idle reducers take few issue slots and memory requests from
+//     the producer beside them; the other waves wait at the workgroup
+//     barrier, which needs no LDS.
+//   * After the barrier every wave reads the flags once itself and acquires,
+//     then reduces its own quarter of the tile (32 rows, 16-byte lanes, one
+//     vector of every contribution in flight per lane).
+//   * No wave leaves early, so every wave reaches every barrier.  After a
+//     timeout (recorded in the status word) wave 0 stops waiting; the output
+//     of such a call is undefined.
+template <int NP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void tile_reducer_shared(ReduceArgs a) {
+  const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
+  const int Q = tiles_per_partition(a.M, a.N, NP);
+  const int tiles_n = a.N / kTile;
+  const int ntiles = (a.M / kTile) * tiles_n;
+  const ConsumerSeq seq = consumer_seq(a.dest, NP, a.x, blockIdx.x);
+  const int chunk_rows = a.M / NP;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool poller = lane < NP;
+  const int epoch = static_cast<int>(a.epoch);
+
+  auto global_tile = [&](int t) {
+    int tr, tc;
+    tile_of_number(seq.part, t, grid, &tr, &tc);
+    return tr * tiles_n + tc;
+  };
+  auto flag_of = [&](int gt) {
+    return lane == 0 ? a.flags + gt : a.peer_flags + static_cast<int64_t>(lane - 1) * ntiles + gt;
+  };
+  if (a.publish_peers && wave == 0 && lane >= 1 && lane < NP && lane - 1 != a.withhold_peer) {
+    for (int tt = seq.first; tt < Q; tt += seq.stride)
+      publish_relaxed(const_cast<int*>(a.peer_flags) + static_cast<int64_t>(lane - 1) * ntiles + global_tile(tt),
+                      a.epoch);
+  }
+
+  bool timed_out = false;   // wave 0 only
+  for (int t = seq.first; t < Q; t += seq.stride) {
+    const int gt = global_tile(t);
+    if (wave == 0 && !timed_out) {
+      bool ready = !poller || poll_relaxed(flag_of(gt)) == epoch;
+      const uint64_t deadline = wall_clock64() + a.timeout_ticks;
+      while (__ballot(!ready) != 0) {
+        if (wall_clock64() > deadline) {
+          const int first = __builtin_ctzll(__ballot(!ready));
+          if (lane == 0 && atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
+            atomicExch(a.status + 1, gt);
+            atomicExch(a.status + 2, first == 0 ? -1 : first - 1);
+          }
+          timed_out = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(8);
+        if (!ready) ready = poll_relaxed(flag_of(gt)) == epoch;
+      }
+    }
+    __builtin_amdgcn_s_barrier();
+    // This wave's own observation of the (monotonic) flags, then acquire.
+    if (poller) (void)poll_relaxed(flag_of(gt));
+    acquire_fence();
+
+    const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile + wave * 32;
+    const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
+    const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * chunk_rows : grow0;
+    // Byte offsets fit 32 bits (checked on the host), so each load is a
+    // wave-uniform base plus one per-lane offset register.
+#pragma unroll 1
+    for (int i = 0; i < 8; ++i) {
+      const int v = lane + 64 * i;
+      const int64_t r = v >> 4, cc = (v & 15) * 8;
+      const uint32_t offc = static_cast<uint32_t>(((grow0 + r) * a.ldc + gcol0 + cc) * 2);
+      const uint32_t offp = static_cast<uint32_t>(((grow0 + r) * a.ldp + gcol0 + cc) * 2);
+      const r_u32x4_t lv = ld_stream_at(a.partial, offc);
+      r_u32x4_t pv[NP > 1 ? NP - 1 : 1];
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q) pv[q] = ld_stream_at(a.peers[q], offp);
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = __builtin_bit_cast(float, lv[e] << 16);
+        acc[2 * e + 1] = __builtin_bit_cast(float, lv[e] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __builtin_bit_cast(float, pv[q][e] << 16);
+          acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][e] & 0xffff0000u);
+        }
+      r_u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+      const uint32_t offo = static_cast<uint32_t>(((orow0 + r) * a.ldo + gcol0 + cc) * 2);
+      __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(reinterpret_cast<char*>(a.out) + offo));
+    }
+  }
 }
 
 // Publishes the synthetic peers' flags for this call (they stand in for the

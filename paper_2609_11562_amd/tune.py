@@ -82,7 +82,7 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
             kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, record_timing=1)
             cfg = E.Config.make(**kw)
             if E.validate(M, N, K, P, E.DEST_ALL if scope == "all" else 0, cfg) != E.OK:
-                continue
+                continue   # e.g. a block that does not divide the chunk, or x = -1 with two streams
             wall, e2e = _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs)
             row = {k: v for k, v in kw.items() if k != "record_timing"}
             row.update(order=E.ORDER_INTERLEAVED, wall_ms=round(wall, 5), event_ms=round(e2e, 5),

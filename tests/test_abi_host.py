@@ -71,7 +71,11 @@ def test_validate_config(lib):
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_threads=64)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(withhold_peer=1)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(withhold_peer=0)) == E.OK
-    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=3)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=2)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-1)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-1, launch=1)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-2)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=1)) == E.OK
 
 

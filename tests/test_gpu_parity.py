@@ -135,12 +135,18 @@ def test_results_independent_of_order_budget_threads_and_mode():
                    [dict(reduce_wgs=x) for x in (4, 8, 32, 64)] + \
                    [dict(reduce_threads=b) for b in (128, 512)] + \
                    [dict(launch=1), dict(launch=1, reduce_threads=512, reduce_wgs=8),
-                    dict(launch=1, gemm_cfg=3, reduce_threads=1024)]
+                    dict(launch=1, gemm_cfg=3, reduce_threads=1024)] + \
+                   [dict(launch=2), dict(launch=2, reduce_wgs=5), dict(launch=2, gemm_cfg=1, reduce_wgs=40)] + \
+                   [dict(reduce_wgs=-1), dict(reduce_wgs=-1, gemm_cfg=3)]
         for kw in variants:
             o = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(**kw)))
             assert np.array_equal(o, base), kw
         seq = host_bits(run(ctx, A, B, peers, E.DEST_ALL, fused=False))
         assert np.array_equal(seq, base), "sequential differs from fused"
+        # x = -1 (no dedicated reducers) is a fused-launch setting; the
+        # standalone reducer of the sequential form falls back to its default.
+        seq = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(reduce_wgs=-1), fused=False))
+        assert np.array_equal(seq, base), "sequential with reduce_wgs=-1 differs"
         parts = [host_bits(run(ctx, A, B, peers, d, E.Config.make(reduce_wgs=x)))
                  for d, x in zip(range(P), (1, 3, 16, 64))]
         assert np.array_equal(np.concatenate(parts, axis=0), base), "chunks differ from all-chunk output"
@@ -161,8 +167,8 @@ def test_reducer_is_exact_on_given_partial():
         absab = np.abs(oracle.bf16_to_f64(prob.A)) @ np.abs(oracle.bf16_to_f64(prob.B))
         err = np.abs(oracle.bf16_to_f64(pbits) - C)
         assert np.all(err <= 2 * 2.0 ** -8 * np.abs(C) + 2 * 2.0 ** -24 * K * absab)
-        for dest in (3, E.DEST_ALL):
-            o = ctx.reduce_only(partial, peers, dest)
+        for dest, cfg in ((3, None), (E.DEST_ALL, None), (2, E.Config.make(reduce_wgs=-1))):
+            o = ctx.reduce_only(partial, peers, dest, cfg=cfg)
             assert ctx.query_status()[0] == E.OK
             rows = out_global_rows(M, P, dest)
             want = oracle.reduce_scatter.reduce_tile_f32(pbits[rows], [p[rows] for p in prob.peers])
@@ -173,7 +179,7 @@ def test_reducer_is_exact_on_given_partial():
 def test_withheld_peer_times_out_then_recovers(tiny):
     w, prob, ctx, (A, B, peers) = tiny
     print("[timeout]", flush=True)
-    for launch in (0, 1):
+    for launch in (0, 1, 2):
         cfg = E.Config.make(withhold_peer=0, timeout_us=20000, reduce_wgs=2, launch=launch)
         ctx.gemm_rs(A, B, peers, 1, cfg=cfg, reduce_stream=torch.cuda.Stream())
         st, tile, src = ctx.query_status()
@@ -202,7 +208,7 @@ def test_poisoned_buffers_never_leak_across_repeated_calls():
             partial.fill_(nan)
             out.fill_(nan)
             ctx.gemm_rs(A, B, peers, 5, out=out, partial=partial, reduce_stream=rs,
-                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 2))
+                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 3))
             got = host_bits(out)
             if i < 2:
                 check_rows(probs[i], got, out_global_rows(M, P, 5))
