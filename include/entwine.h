@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define ENTWINE_ABI_VERSION 1
+#define ENTWINE_ABI_VERSION 2
 #define ENTWINE_TILE 128      /* side of a reduction tile (Section 4.2) */
 #define ENTWINE_MAX_P 8       /* chunk count supported (the paper's W <= 8) */
 #define ENTWINE_DEST_ALL (-1) /* reduce every chunk (one-GPU emulation) */
@@ -107,6 +107,14 @@ typedef struct {
                              on every CU and x small reducer workgroups of
                              256 threads beside it (default x: one per CU);
                              1 and 0 partition the CUs instead */
+  int32_t release_blocks; /* g: a producer workgroup publishes its finished
+                             tiles after every g of its blocks, one release
+                             fence each time (Section 5.3.2, release
+                             granularity); 0 = default = 1; -1 = only once,
+                             after its last block */
+  int32_t store_mode;     /* partial tile stores: 0 = write-through (the
+                             release has little dirty data to write back),
+                             1 = non-temporal (written back by the release) */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */

@@ -111,7 +111,8 @@ struct Resolved {
   // x: dedicated reducer workgroups of the fused launch (0 with reduce_wgs
   // -1); x_alone: grid of the standalone reducer kernel (reduce_only, the
   // sequential form and the two-stream forms), never 0.
-  int order, gemm_cfg, BM, BN, x, x_alone, threads, withhold, timing, group_m, gemm_wgs, launch;
+  int order, gemm_cfg, BM, BN, x, x_alone, threads, withhold, timing, group_m, gemm_wgs, launch, release_blocks,
+      store_mode;
   uint64_t timeout_us;
 };
 
@@ -134,6 +135,8 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
   if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
   if (c.launch < 0 || c.launch > 2) return fail(ctx, ENTWINE_EINVAL, "launch must be 0, 1 or 2");
+  if (c.release_blocks < -1) return fail(ctx, ENTWINE_EINVAL, "release_blocks must be >= -1");
+  if (c.store_mode < 0 || c.store_mode > 1) return fail(ctx, ENTWINE_EINVAL, "store_mode must be 0 or 1");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -162,6 +165,8 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->group_m = c.group_m ? c.group_m : 4;
   r->gemm_wgs = c.gemm_wgs;
   r->launch = c.launch;
+  r->release_blocks = c.release_blocks == 0 ? 1 : c.release_blocks;   // -1 (or any g < 1): at the end
+  r->store_mode = c.store_mode;
   return ENTWINE_OK;
 }
 
@@ -287,6 +292,8 @@ GemmArgs gemm_args(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t l
   g.group_m = r.group_m;
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
+  g.release_blocks = r.release_blocks;
+  g.nt_stores = r.store_mode;
   return g;
 }
 
@@ -380,7 +387,8 @@ entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs&
                             int64_t ldo, uint32_t epoch, TimingSlot* ts, hipStream_t s) {
   ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
   ra.task_ctr = ctx->task_ctr;
-  ra.ntasks = tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
+  // Dynamic tasks are half-tiles (reducer_dynamic).
+  ra.ntasks = 2 * tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
   const int G = producer_grid(ctx, r, true);
   const int grid = G + r.x;
   unsigned long long* stamps = nullptr;
@@ -427,6 +435,8 @@ void entwine_config_default(entwine_config* cfg) {
   cfg->group_m = 0;
   cfg->gemm_wgs = 0;
   cfg->launch = 0;
+  cfg->release_blocks = 0;
+  cfg->store_mode = 0;
 }
 
 int32_t entwine_abi_version(void) { return ENTWINE_ABI_VERSION; }

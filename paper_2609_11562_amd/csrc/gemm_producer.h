@@ -76,6 +76,8 @@ struct GemmArgs {
   int M, N, K, P, order, group_m;
   int* flags;             // one per global 128 x 128 tile, row-major; null = no publish
   uint32_t epoch;
+  int release_blocks;     // publish after every g blocks (g >= 1), or only after the last (g <= 0)
+  int nt_stores;          // 1: non-temporal tile stores (written back at the release); 0: write-through
 };
 
 template <int BM_, int BN_>
@@ -450,6 +452,7 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
   char* const cst = smem + NS * S::STAGE + wave * (32 * ROWB);
 
   int g = 0;
+  int unpublished = 0;   // first of this workgroup's blocks whose tiles are not yet published
   for (int lb = 0; lb < mine; ++lb) {
     const BlockPos bp = block_of_position(a.order, w + lb * G, grid);
 #pragma unroll
@@ -488,23 +491,33 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
       for (int r0 = 0; r0 < 32; r0 += RPI) {
         const int rr = r0 + lane / CPR, c = lane % CPR;
         const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + rr * ROWB + ((c ^ (rr % CPR)) << 4));
-        store16_wt(cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8, v);
+        uint16_t* dst = cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8;
+        if (a.nt_stores) __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(dst));
+        else store16_wt(dst, v);
       }
       wave_sync();                               // the next round rewrites these rows
     }
 
-    if (a.flags != nullptr) {
+    // Release granularity (paper Section 5.3.2): one fence covers the tiles
+    // of every block since the last publication.
+    const bool release = a.flags != nullptr &&
+                         (lb + 1 == mine || (a.release_blocks >= 1 && lb + 1 - unpublished >= a.release_blocks));
+    if (release) {
       __syncthreads();
       if (tid == 0) {
         const int tiles_n = a.N / kTile;
         release_fence();
+        for (int pb = unpublished; pb <= lb; ++pb) {
+          const BlockPos pp = pb == lb ? bp : block_of_position(a.order, w + pb * G, grid);
 #pragma unroll
-        for (int ti = 0; ti < BM / kTile; ++ti)
+          for (int ti = 0; ti < BM / kTile; ++ti)
 #pragma unroll
-          for (int tj = 0; tj < BN / kTile; ++tj)
-            publish_relaxed(a.flags + (bp.mb * (BM / kTile) + ti) * tiles_n + bp.nb * (BN / kTile) + tj,
-                            a.epoch);
+            for (int tj = 0; tj < BN / kTile; ++tj)
+              publish_relaxed(a.flags + (pp.mb * (BM / kTile) + ti) * tiles_n + pp.nb * (BN / kTile) + tj,
+                              a.epoch);
+        }
       }
+      unpublished = lb + 1;
     }
   }
   // Loads past the end of the stream may still be writing LDS.

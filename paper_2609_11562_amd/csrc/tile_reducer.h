@@ -104,18 +104,20 @@ __device__ __forceinline__ bool wave_await_tile(const ReduceArgs& a, int gt, int
   return true;
 }
 
-// Reduces global tile gt with THREADS threads: every element starts from the
-// local contribution, the peers are added in rank order in fp32, the result
-// is rounded to bf16 and stored once.  G vectors of every contribution are
-// loaded per lane before any is consumed; `after_first_loads` runs right
-// after the first batch of loads is issued (used to overlap a flag poll).
-template <int THREADS, int NP, typename Hook>
-__device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int tiles_n, Hook after_first_loads) {
-  constexpr int VPT = (kTile * kTile * 2 / 16) / THREADS;  // 16-byte vectors per thread
-  constexpr int GMAX = 32 / NP;                             // loads in flight per lane <= 32
+// Reduces ROWS rows of global tile gt, starting at row `row0` of the tile,
+// with THREADS threads: every element starts from the local contribution,
+// the peers are added in rank order in fp32, the result is rounded to bf16
+// and stored once.  G vectors of every contribution are loaded per lane
+// before any is consumed (at most MAXLOADS loads in flight per lane);
+// `after_first_loads` runs right after the first batch of loads is issued
+// (used to overlap a flag poll).
+template <int THREADS, int NP, int ROWS = kTile, int MAXLOADS = 32, typename Hook>
+__device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int tiles_n, int row0, Hook after_first_loads) {
+  constexpr int VPT = (ROWS * kTile * 2 / 16) / THREADS;   // 16-byte vectors per thread
+  constexpr int GMAX = MAXLOADS / NP;                       // loads in flight per lane <= MAXLOADS
   constexpr int G = pow2_floor(VPT < GMAX ? VPT : GMAX);    // vectors per batch
-  static_assert(VPT % G == 0, "batch must divide the per-thread vectors");
-  const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile;
+  static_assert(VPT >= 1 && VPT % G == 0, "batch must divide the per-thread vectors");
+  const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile + row0;
   const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
   const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * (a.M / NP) : grow0;
 #pragma unroll
@@ -202,7 +204,7 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
     const int gtn = tn < Q ? global_tile(tn) : 0;
     seen = epoch;
     // The first poll of the next tile's flags rides behind this tile's loads.
-    reduce_tile<THREADS, NP>(a, gt, tiles_n, [&] {
+    reduce_tile<THREADS, NP>(a, gt, tiles_n, 0, [&] {
       if (poller && tn < Q) seen = poll_relaxed(flag_of_lane(a, lane, ntiles, gtn));
     });
     if (tn >= Q) break;
@@ -213,30 +215,33 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
 }
 
 // Publishes, as part of one launch, the synthetic peers' flags of every tile
-// the call reduces (`ntasks` tiles in consumer order, see task_tile), split
-// over all nb workgroups; peer `withhold_peer` stays unpublished.
+// the call reduces (a.ntasks / 2 tiles: the dynamic tasks are half-tiles),
+// split over all nb workgroups; peer `withhold_peer` stays unpublished.
 __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, int b, int nb) {
   const BlockGrid grid = make_grid(a.M, a.N, np, a.BM, a.BN, a.group_m);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
-  const int64_t n = static_cast<int64_t>(np - 1) * a.ntasks;
+  const int call_tiles = a.ntasks / 2;
+  const int64_t n = static_cast<int64_t>(np - 1) * call_tiles;
   for (int64_t i = static_cast<int64_t>(b) * blockDim.x + threadIdx.x; i < n;
        i += static_cast<int64_t>(nb) * blockDim.x) {
-    const int q = static_cast<int>(i / a.ntasks), task = static_cast<int>(i % a.ntasks);
+    const int q = static_cast<int>(i / call_tiles), u = static_cast<int>(i % call_tiles);
     if (q == a.withhold_peer) continue;
-    const int part = a.dest >= 0 ? a.dest : task % np;
-    const int idx = a.dest >= 0 ? task : task / np;
+    const int part = a.dest >= 0 ? a.dest : u % np;
+    const int idx = a.dest >= 0 ? u : u / np;
     int tr, tc;
     tile_of_number(part, idx, grid, &tr, &tc);
     publish_relaxed(const_cast<int*>(a.peer_flags) + static_cast<int64_t>(q) * ntiles + tr * tiles_n + tc, a.epoch);
   }
 }
 
-// The reducer role with dynamic tasks: workgroups take tiles from a device
-// counter in consumer order (task t is tile t of the destination's
-// partition; with every destination, tile t / P of partition t % P, which
-// interleaves the partitions as Equation 1 does), so the dedicated reducers
-// and every producer that has finished its blocks share the remaining tiles.
+// The reducer role with dynamic tasks: workgroups take half-tiles from a
+// device counter in consumer order (task t is half t % 2 of tile u = t / 2
+// of the destination's partition; with every destination, tile u / P of
+// partition u % P, which interleaves the partitions as Equation 1 does), so
+// the dedicated reducers and every producer that has finished its blocks
+// share the remaining work; half-tiles keep every workgroup busy when a
+// chunk has fewer tiles than the device has CUs.
 // Each workgroup ends with one failed take; the last workgroup of the grid to
 // finish returns both counters to zero, ready for the next call.  After a
 // timeout waits are skipped (the call's output is then undefined) but the
@@ -248,8 +253,9 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
   const int ntiles = (a.M / kTile) * tiles_n;
   const int lane = threadIdx.x & 63;
   auto task_tile = [&](int task) {
-    const int part = a.dest >= 0 ? a.dest : task % NP;
-    const int idx = a.dest >= 0 ? task : task / NP;
+    const int u = task >> 1;
+    const int part = a.dest >= 0 ? a.dest : u % NP;
+    const int idx = a.dest >= 0 ? u : u / NP;
     int tr, tc;
     tile_of_number(part, idx, grid, &tr, &tc);
     return tr * tiles_n + tc;
@@ -271,7 +277,7 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
     }
     __syncthreads();
     const int next = s[1];
-    reduce_tile<THREADS, NP>(a, gt, tiles_n, [] {});
+    reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, (task & 1) * (kTile / 2), [] {});
     __syncthreads();   // s[1] is rewritten next
     task = next;
   }

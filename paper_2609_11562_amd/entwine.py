@@ -38,7 +38,8 @@ class Config(ctypes.Structure):
                 ("reduce_wgs", ctypes.c_int32), ("reduce_threads", ctypes.c_int32),
                 ("timeout_us", ctypes.c_int32), ("withhold_peer", ctypes.c_int32),
                 ("record_timing", ctypes.c_int32), ("group_m", ctypes.c_int32),
-                ("gemm_wgs", ctypes.c_int32), ("launch", ctypes.c_int32)]
+                ("gemm_wgs", ctypes.c_int32), ("launch", ctypes.c_int32),
+                ("release_blocks", ctypes.c_int32), ("store_mode", ctypes.c_int32)]
 
     @classmethod
     def make(cls, **kw) -> "Config":

@@ -58,7 +58,8 @@ def _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, 
 
 
 def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs=DEFAULT_CFGS,
-          group_ms=DEFAULT_GROUP_M, steps: int = 30, warmup: int = 10, launch: int = 0, log=None):
+          group_ms=DEFAULT_GROUP_M, steps: int = 30, warmup: int = 10, launch: int = 0, release_blocks=(1,),
+          log=None):
     """Time every valid configuration; returns (best, rows) where rows are
     dicts with the configuration, wall ms per call and median event time.
     With launch 0 (one kernel, reducers of 256 threads) b has no effect and
@@ -78,8 +79,9 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
         outs = {d: torch.empty(ctx.out_rows(d), N, dtype=torch.bfloat16, device="cuda") for d in dests}
         gs = torch.cuda.current_stream()
         rs = torch.cuda.Stream()
-        for gc, x, b, gm in itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms):
-            kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, record_timing=1)
+        for gc, x, b, gm, g in itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms, release_blocks):
+            kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, release_blocks=g,
+                      record_timing=1)
             cfg = E.Config.make(**kw)
             if E.validate(M, N, K, P, E.DEST_ALL if scope == "all" else 0, cfg) != E.OK:
                 continue   # e.g. a block that does not divide the chunk, or x = -1 with two streams
@@ -99,7 +101,7 @@ def write_entry(workload: str, scope: str, best: dict, path: str = _TABLE) -> No
     if os.path.exists(path):
         with open(path) as f:
             table = json.load(f)
-    keep = ("order", "gemm_cfg", "reduce_wgs", "reduce_threads", "group_m", "launch")
+    keep = ("order", "gemm_cfg", "reduce_wgs", "reduce_threads", "group_m", "launch", "release_blocks")
     table.setdefault(workload, {})[scope] = {k: best[k] for k in keep}
     table[workload][scope]["measured_ms"] = best["wall_ms"]
     with open(path, "w") as f:
@@ -117,14 +119,15 @@ def main(argv=None):
     ap.add_argument("--group-m", default=",".join(map(str, DEFAULT_GROUP_M)))
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--launch", type=int, default=0, help="0 = one kernel launch, 1 = two streams")
+    ap.add_argument("--launch", type=int, default=0, help="0 = one kernel launch, 1 = two streams, 2 = shared pool")
+    ap.add_argument("--release-blocks", default="1", help="release granularities g to try (-1 = once per workgroup)")
     ap.add_argument("--write", action="store_true", help="record the winners in the table")
     ap.add_argument("--table", default=_TABLE, help="JSON table to update (default: the package's tuned.json)")
     a = ap.parse_args(argv)
     ints = lambda s: tuple(int(v) for v in s.split(","))
     for wl in a.workload:
         best, _ = sweep(wl, a.scope, ints(a.xs), ints(a.bs), ints(a.cfgs), ints(a.group_m), a.steps, a.warmup,
-                        a.launch, log=lambda s: print(s, flush=True))
+                        a.launch, ints(a.release_blocks), log=lambda s: print(s, flush=True))
         print(json.dumps({"workload": wl, "scope": a.scope, "best": best}), flush=True)
         if a.write:
             write_entry(wl, a.scope, best, a.table)

@@ -13,7 +13,7 @@ import json
 import os
 
 _TABLE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tuned.json")
-_FIELDS = ("order", "gemm_cfg", "reduce_wgs", "reduce_threads", "group_m", "launch")
+_FIELDS = ("order", "gemm_cfg", "reduce_wgs", "reduce_threads", "group_m", "launch", "release_blocks", "store_mode")
 
 
 def load_table() -> dict:

@@ -39,7 +39,8 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_strings(lib):
-    assert lib.entwine_abi_version() == 1
+    assert lib.entwine_abi_version() == 2
+    assert ctypes.sizeof(E.Config) == 12 * 4
     assert E._status_name(E.ETIMEOUT) == "ENTWINE_ETIMEOUT"
     c = E.Config.make()
     assert (c.order, c.gemm_cfg, c.withhold_peer) == (E.ORDER_INTERLEAVED, -1, -1)
@@ -76,6 +77,9 @@ def test_validate_config(lib):
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-1)) == E.OK
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-1, launch=1)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-1, store_mode=1)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(store_mode=2)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=1)) == E.OK
 
 

@@ -27,7 +27,7 @@ def test_missing_workload_falls_back_to_defaults():
 
 def test_write_entry_round_trip(tmp_path):
     path = tmp_path / "t.json"
-    best = dict(order=0, gemm_cfg=1, reduce_wgs=24, reduce_threads=512, group_m=4, launch=0, wall_ms=0.5,
+    best = dict(order=0, gemm_cfg=1, reduce_wgs=24, reduce_threads=512, group_m=4, launch=0, release_blocks=1, wall_ms=0.5,
                 event_ms=0.4)
     tune.write_entry("llama7b_mlp_down_tp8", "rank", best, str(path))
     tune.write_entry("llama7b_mlp_down_tp8", "all", dict(best, reduce_wgs=32), str(path))
