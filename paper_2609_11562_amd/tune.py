@@ -10,7 +10,9 @@ winner in ``tuned.json`` (read back by :func:`tuning.tuned_config`).
 Timing follows the benchmark: synthetic seeded inputs resident on the device,
 ``warmup`` untimed calls, then ``steps`` calls whose wall time (host clock
 around a synchronised batch) gives ms per call; the destination chunk cycles
-through 0 .. P-1 in rank scope.
+through 0 .. P-1 in rank scope.  The engine clock drifts with power and
+temperature, so the whole grid is timed ``passes`` times and each
+configuration keeps its best pass.
 
     python -m paper_2609_11562_amd.tune --workload llama70b_attn_out_tp8 --write
 """
@@ -59,7 +61,7 @@ def _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, 
 
 def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs=DEFAULT_CFGS,
           group_ms=DEFAULT_GROUP_M, steps: int = 30, warmup: int = 10, launch: int = 0, release_blocks=(1,),
-          log=None):
+          passes: int = 2, log=None):
     """Time every valid configuration; returns (best, rows) where rows are
     dicts with the configuration, wall ms per call and median event time.
     With launch 0 (one kernel, reducers of 256 threads) b has no effect and
@@ -72,28 +74,32 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
     A = bits_to_torch(prob.A).cuda()
     B = bits_to_torch(prob.B).cuda()
     peers = [bits_to_torch(p).cuda() for p in prob.peers]
-    rows = []
+    rows = {}
     with E.Context(M, N, K, P) as ctx:
         partial = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
         dests = [E.DEST_ALL] if scope == "all" else list(range(P))
         outs = {d: torch.empty(ctx.out_rows(d), N, dtype=torch.bfloat16, device="cuda") for d in dests}
         gs = torch.cuda.current_stream()
         rs = torch.cuda.Stream()
-        for gc, x, b, gm, g in itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms, release_blocks):
-            kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, release_blocks=g,
-                      record_timing=1)
-            cfg = E.Config.make(**kw)
-            if E.validate(M, N, K, P, E.DEST_ALL if scope == "all" else 0, cfg) != E.OK:
-                continue   # e.g. a block that does not divide the chunk, or x = -1 with two streams
-            wall, e2e = _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs)
-            row = {k: v for k, v in kw.items() if k != "record_timing"}
-            row.update(order=E.ORDER_INTERLEAVED, wall_ms=round(wall, 5), event_ms=round(e2e, 5),
-                       tflops=round(2.0 * M * N * K / (wall * 1e-3) / 1e12, 1))
-            rows.append(row)
-            if log:
-                log(json.dumps(row))
-    best = min(rows, key=lambda r: r["wall_ms"])
-    return best, rows
+        grid = list(itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms, release_blocks))
+        for _ in range(passes):
+            for gc, x, b, gm, g in grid:
+                kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, release_blocks=g,
+                          record_timing=1)
+                cfg = E.Config.make(**kw)
+                if E.validate(M, N, K, P, E.DEST_ALL if scope == "all" else 0, cfg) != E.OK:
+                    continue   # e.g. a block that does not divide the chunk, or x = -1 with two streams
+                wall, e2e = _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs)
+                row = {k: v for k, v in kw.items() if k != "record_timing"}
+                row.update(order=E.ORDER_INTERLEAVED, wall_ms=round(wall, 5), event_ms=round(e2e, 5),
+                           tflops=round(2.0 * M * N * K / (wall * 1e-3) / 1e12, 1))
+                key = (gc, x, b, gm, g)
+                if key not in rows or row["wall_ms"] < rows[key]["wall_ms"]:
+                    rows[key] = row
+                if log:
+                    log(json.dumps(row))
+    best = min(rows.values(), key=lambda r: r["wall_ms"])
+    return best, list(rows.values())
 
 
 def write_entry(workload: str, scope: str, best: dict, path: str = _TABLE) -> None:
@@ -121,13 +127,14 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--launch", type=int, default=0, help="0 = one kernel launch, 1 = two streams, 2 = shared pool")
     ap.add_argument("--release-blocks", default="1", help="release granularities g to try (-1 = once per workgroup)")
+    ap.add_argument("--passes", type=int, default=2, help="times the grid is timed; each configuration keeps its best")
     ap.add_argument("--write", action="store_true", help="record the winners in the table")
     ap.add_argument("--table", default=_TABLE, help="JSON table to update (default: the package's tuned.json)")
     a = ap.parse_args(argv)
     ints = lambda s: tuple(int(v) for v in s.split(","))
     for wl in a.workload:
         best, _ = sweep(wl, a.scope, ints(a.xs), ints(a.bs), ints(a.cfgs), ints(a.group_m), a.steps, a.warmup,
-                        a.launch, ints(a.release_blocks), log=lambda s: print(s, flush=True))
+                        a.launch, ints(a.release_blocks), a.passes, log=lambda s: print(s, flush=True))
         print(json.dumps({"workload": wl, "scope": a.scope, "best": best}), flush=True)
         if a.write:
             write_entry(wl, a.scope, best, a.table)
