@@ -10,8 +10,10 @@ imports nothing from the product.
   error bound and the paper's tolerance gate.
 * ``schedule``: Equation 1 and the comparison traversal orders, tile
   numbering and the consumer task assignment.
+* ``layer``: the layer epilogue (residual addition and RMSNorm) and its
+  rounding bounds.
 """
-from . import reduce_scatter, schedule  # noqa: F401
+from . import layer, reduce_scatter, schedule  # noqa: F401
 from .reduce_scatter import (  # noqa: F401
     bf16_to_f64, chunk_rows, error_bound_rows, gemm_reduce_scatter, local_partial,
     output_rows, paper_gate, reduce_chunk)

@@ -92,7 +92,7 @@ def output_rows(A_bits, B_bits, peer_bits, rows) -> np.ndarray:
     return C
 
 
-def error_bound_rows(A_bits, B_bits, peer_bits, rows) -> np.ndarray:
+def error_bound_rows(A_bits, B_bits, peer_bits, rows, final_rounding: bool = True) -> np.ndarray:
     """Elementwise rounding-error bound for a path that (1) accumulates the
     GEMM in float32, (2) stores the local partial as bfloat16, (3) sums the
     partial and the peers in float32 and (4) rounds the result to bfloat16.
@@ -103,6 +103,8 @@ def error_bound_rows(A_bits, B_bits, peer_bits, rows) -> np.ndarray:
         (3) (P-1) u32 (|C| + sum|Pi|)   (4) u16 |O|
     It is returned doubled to absorb second-order terms:
         2 u16 (|O| + |C|) + 2 u32 (K |A||B| + P (|C| + sum|Pi|)).
+    With ``final_rounding`` False, term (4) is left out: the bound on the
+    float32 sum itself, for paths that keep computing with it.
     """
     rows = np.asarray(rows, dtype=np.int64)
     a = bf16_to_f64(np.asarray(A_bits)[rows])
@@ -117,7 +119,7 @@ def error_bound_rows(A_bits, B_bits, peer_bits, rows) -> np.ndarray:
         v = bf16_to_f64(np.asarray(pb)[rows])
         O += v
         abs_peers += np.abs(v)
-    return 2 * U_BF16 * (np.abs(O) + np.abs(C)) + 2 * U_F32 * (
+    return 2 * U_BF16 * ((np.abs(O) if final_rounding else 0.0) + np.abs(C)) + 2 * U_F32 * (
         K * absAB + P * (np.abs(C) + abs_peers))
 
 
