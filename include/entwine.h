@@ -149,6 +149,28 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
 
 /* Producer alone (flags still published): partial = bf16(A B).  Used for
  * the uncontended GEMM time of the overlap-efficiency metric (Appendix C). */
+/* The fused path followed by the layer epilogue of the paper's layer-level
+ * evaluation (Section 5.2: residual addition and RMSNorm after the
+ * reduce-scatter), as one launch on `stream` (cfg->launch must be 0, else
+ * ENTWINE_EUNSUPPORTED).  For every output row i of the destination
+ * (rows as `out` of entwine_gemm_rs):
+ *   h[i,:] = bf16(sum + residual[i,:])   the reduced row plus the residual,
+ *                                        added in fp32 after the peers;
+ *   y[i,:] = bf16(h[i,:] * (mean_j h[i,j]^2 + eps)^(-1/2) * gamma)
+ *                                        from the stored bf16 h, fp32 math.
+ * residual, h_out, y_out: bf16, out_rows x N (leading dimensions ldr, ldh,
+ * ldy); gamma: bf16, N; eps > 0 and finite (ENTWINE_EINVAL otherwise).  The
+ * row statistics live in context buffers (a pair, used by alternate calls),
+ * so calls on one context are ordered by their stream.  h is reproducible
+ * bit for bit; y is not (the per-row sums of squares are accumulated with
+ * atomics in a varying order).  Errors as entwine_gemm_rs. */
+entwine_status entwine_gemm_rs_rmsnorm(entwine_ctx* ctx, const void* A, int64_t lda, const void* B,
+                                       int64_t ldb, const void* const* peers, int64_t ldp, int32_t dest,
+                                       const void* residual, int64_t ldr, const void* gamma, float eps,
+                                       void* h_out, int64_t ldh, void* y_out, int64_t ldy,
+                                       void* partial, int64_t ldc, const entwine_config* cfg,
+                                       void* stream);
+
 entwine_status entwine_gemm_only(entwine_ctx* ctx, const void* A, int64_t lda, const void* B,
                                  int64_t ldb, void* partial, int64_t ldc,
                                  const entwine_config* cfg, void* stream);

@@ -30,6 +30,12 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   const unsigned long long t0 = stamps ? wall_clock64() : 0;
   const int b = blockIdx.x;
   publish_peer_slice(r, np, b, gridDim.x);
+  if (r.layer) {   // clear the other statistics buffers for the next layer call
+    for (int64_t i = int64_t(b) * blockDim.x + threadIdx.x; i < r.out_rows; i += int64_t(gridDim.x) * blockDim.x) {
+      r.next_sumsq[i] = 0.0f;
+      if (i % (kTile / 2) == 0) r.next_rows_done[i / (kTile / 2)] = 0u;
+    }
+  }
   if (b < G) producer_body<BM, BN, TAIL>(g, b, G, smem);
   const unsigned long long t1 = stamps ? wall_clock64() : 0;
   int* s = reinterpret_cast<int*>(smem);

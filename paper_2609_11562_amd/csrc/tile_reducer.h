@@ -45,7 +45,22 @@ struct ReduceArgs {
                            // workgroup's tiles before consuming them
   int withhold_peer;       // with publish_peers: peer left unpublished, or -1
   unsigned int* task_ctr;  // dynamic tasks: {next task, finished workgroups}
-  int ntasks;              // dynamic tasks: tiles this call reduces
+  int ntasks;              // dynamic tasks: all tasks of this call
+  // Layer epilogue (residual addition + RMSNorm after the reduce-scatter):
+  // `out` receives the residual stream h = sum + residual, `y` the
+  // normalised rows; tasks [0, ntasks_reduce) reduce, the rest normalise.
+  int layer;
+  int ntasks_reduce;
+  const uint16_t* residual;  // rows like `out`, leading dimension ldr
+  int64_t ldr, ldy;
+  const uint16_t* gamma;     // N weights
+  uint16_t* y;
+  float eps;
+  float* sumsq;              // per output row, zero on entry
+  unsigned int* rows_done;   // per 64 output rows: half-tiles reduced, zero on entry
+  float* next_sumsq;         // the other buffers of the pair, cleared for the next call
+  unsigned int* next_rows_done;
+  int64_t out_rows;
 };
 
 typedef uint32_t r_u32x4_t __attribute__((ext_vector_type(4)));
@@ -124,6 +139,7 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
   for (int v0 = 0; v0 < VPT; v0 += G) {
     r_u32x4_t lv[G];
     r_u32x4_t pv[NP > 1 ? NP - 1 : 1][G];
+    r_u32x4_t rv[G];
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const int v = threadIdx.x + THREADS * (v0 + gi);
@@ -131,6 +147,7 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
       lv[gi] = ld_stream(a.partial + (grow0 + r) * a.ldc + gcol0 + cc);
 #pragma unroll
       for (int q = 0; q < NP - 1; ++q) pv[q][gi] = ld_stream(a.peers[q] + (grow0 + r) * a.ldp + gcol0 + cc);
+      if (a.layer) rv[gi] = ld_stream(a.residual + (orow0 + r) * a.ldr + gcol0 + cc);
     }
     if (v0 == 0) after_first_loads();
 #pragma unroll
@@ -148,13 +165,65 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
           acc[2 * e] += __builtin_bit_cast(float, pv[q][gi][e] << 16);
           acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][gi][e] & 0xffff0000u);
         }
+      if (a.layer) {   // residual stream: the sum plus the residual, in fp32
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __builtin_bit_cast(float, rv[gi][e] << 16);
+          acc[2 * e + 1] += __builtin_bit_cast(float, rv[gi][e] & 0xffff0000u);
+        }
+      }
       r_u32x4_t o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
       const int v = threadIdx.x + THREADS * (v0 + gi);
       const int64_t r = v >> 4, cc = (v & 15) * 8;
       __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc));
+      if (a.layer) {
+        // Sum of squares of the stored (bf16) residual stream for this row:
+        // the 16 lanes holding one row fold their parts, one atomic per row.
+        float ss = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __builtin_bit_cast(float, o[e] << 16);
+          const float hi = __builtin_bit_cast(float, o[e] & 0xffff0000u);
+          ss += lo * lo + hi * hi;
+        }
+        ss += __shfl_xor(ss, 8, 16);
+        ss += __shfl_xor(ss, 4, 16);
+        ss += __shfl_xor(ss, 2, 16);
+        ss += __shfl_xor(ss, 1, 16);
+        if ((threadIdx.x & 15) == 0) unsafeAtomicAdd(a.sumsq + orow0 + r, ss);
+      }
     }
+  }
+}
+
+// Normalises ROWS rows of tile gt starting at tile row `row0` (layer
+// epilogue): y = bf16(h * (mean of squares + eps)^(-1/2) * gamma), h read
+// back as stored, the mean from the completed per-row sums.
+template <int THREADS, int ROWS>
+__device__ __forceinline__ void normalize_rows(const ReduceArgs& a, int gt, int tiles_n, int row0, int np) {
+  constexpr int VPT = (ROWS * kTile * 2 / 16) / THREADS;
+  const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile + row0;
+  const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
+  const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * (a.M / np) : grow0;
+  const float inv_n = 1.0f / static_cast<float>(a.N);
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int v = threadIdx.x + THREADS * i;
+    const int64_t r = v >> 4, cc = (v & 15) * 8;
+    const float rstd = rsqrtf(a.sumsq[orow0 + r] * inv_n + a.eps);
+    const r_u32x4_t h = *reinterpret_cast<const r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc);
+    const r_u32x4_t g = *reinterpret_cast<const r_u32x4_t*>(a.gamma + gcol0 + cc);
+    r_u32x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __builtin_bit_cast(float, h[e] << 16) * rstd * __builtin_bit_cast(float, g[e] << 16);
+      const float hi = __builtin_bit_cast(float, h[e] & 0xffff0000u) * rstd *
+                       __builtin_bit_cast(float, g[e] & 0xffff0000u);
+      o[e] = rnd_pack_bf16x2(lo, hi);
+    }
+    __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.y + (orow0 + r) * a.ldy + gcol0 + cc));
   }
 }
 
@@ -215,13 +284,13 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
 }
 
 // Publishes, as part of one launch, the synthetic peers' flags of every tile
-// the call reduces (a.ntasks / 2 tiles: the dynamic tasks are half-tiles),
+// the call reduces (a.ntasks_reduce / 2 tiles: the reduce tasks are half-tiles),
 // split over all nb workgroups; peer `withhold_peer` stays unpublished.
 __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, int b, int nb) {
   const BlockGrid grid = make_grid(a.M, a.N, np, a.BM, a.BN, a.group_m);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
-  const int call_tiles = a.ntasks / 2;
+  const int call_tiles = a.ntasks_reduce / 2;
   const int64_t n = static_cast<int64_t>(np - 1) * call_tiles;
   for (int64_t i = static_cast<int64_t>(b) * blockDim.x + threadIdx.x; i < n;
        i += static_cast<int64_t>(nb) * blockDim.x) {
@@ -253,7 +322,7 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
   const int ntiles = (a.M / kTile) * tiles_n;
   const int lane = threadIdx.x & 63;
   auto task_tile = [&](int task) {
-    const int u = task >> 1;
+    const int u = (task >= a.ntasks_reduce ? task - a.ntasks_reduce : task) >> 1;
     const int part = a.dest >= 0 ? a.dest : u % NP;
     const int idx = a.dest >= 0 ? u : u / NP;
     int tr, tc;
@@ -267,17 +336,51 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
   bool timed_out = false;   // wave 0
   while (task < a.ntasks) {
     const int gt = task_tile(task);
+    const int row0 = (task & 1) * (kTile / 2);
+    const bool normalise = task >= a.ntasks_reduce;
+    // Layer epilogue: the 64 output rows of this half-tile, counted in
+    // rows_done once reduced in every tile column.
+    const int64_t hrow = (gt / tiles_n) * kTile + row0 - (a.dest >= 0 ? int64_t(a.dest) * (a.M / NP) : 0);
+    unsigned int* const done = a.layer ? a.rows_done + hrow / (kTile / 2) : nullptr;
     if (threadIdx.x < 64) {
       if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
       if (!timed_out) {
-        const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
-        timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
+        if (!normalise) {
+          const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
+          timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
+        } else if (lane == 0) {
+          // every tile column of these rows reduced (so their sums are complete)
+          const uint64_t deadline = wall_clock64() + a.timeout_ticks;
+          while (__hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < static_cast<unsigned>(tiles_n)) {
+            if (wall_clock64() > deadline) {
+              if (atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
+                atomicExch(a.status + 1, gt);
+                atomicExch(a.status + 2, -3);   // -3: row statistics incomplete
+              }
+              timed_out = true;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(8);
+          }
+        }
+        timed_out = __shfl(timed_out, 0);
       }
       if (lane == 0) acquire_fence();
     }
     __syncthreads();
     const int next = s[1];
-    reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, (task & 1) * (kTile / 2), [] {});
+    if (!normalise) {
+      reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, row0, [] {});
+      if (a.layer) {
+        __syncthreads();   // every lane's stores and row sums issued
+        if (threadIdx.x == 0) {
+          release_fence();
+          __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    } else {
+      normalize_rows<THREADS, kTile / 2>(a, gt, tiles_n, row0, NP);
+    }
     __syncthreads();   // s[1] is rewritten next
     task = next;
   }

@@ -59,6 +59,9 @@ _PROTOS = {
     "entwine_ctx_destroy": (_i32, [_vp]),
     "entwine_gemm_rs": (_i32, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_vp), _i64, _i32, _vp, _i64,
                                _vp, _i64, ctypes.POINTER(Config), _vp, _vp]),
+    "entwine_gemm_rs_rmsnorm": (_i32, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_vp), _i64, _i32, _vp, _i64, _vp,
+                                       ctypes.c_float, _vp, _i64, _vp, _i64, _vp, _i64, ctypes.POINTER(Config),
+                                       _vp]),
     "entwine_gemm_only": (_i32, [_vp, _vp, _i64, _vp, _i64, _vp, _i64, ctypes.POINTER(Config), _vp]),
     "entwine_reduce_only": (_i32, [_vp, _vp, _i64, ctypes.POINTER(_vp), _i64, _i32, _vp, _i64,
                                    ctypes.POINTER(Config), _vp]),
@@ -214,6 +217,29 @@ class Context:
         _check(lib().entwine_gemm_rs(self._h, a, lda, b, ldb, parr, ldp, dest, o, ldo, c or None, ldc,
                                      ctypes.byref(cfg) if cfg else None, gs, rs), self._h)
         return out
+
+    def gemm_rs_rmsnorm(self, A, B, peers, dest: int, residual, gamma, eps: float, h_out=None, y_out=None,
+                        partial=None, cfg: Config | None = None, stream=None):
+        """Fused GEMM + tile reduce + residual addition + RMSNorm (one
+        launch); returns ``(h_out, y_out)``."""
+        import torch
+        a, lda = _mat(A, self.M, self.K, "A")
+        b, ldb = _mat(B, self.K, self.N, "B")
+        rows = self.out_rows(dest)
+        if h_out is None:
+            h_out = torch.empty(rows, self.N, dtype=torch.bfloat16, device=A.device)
+        if y_out is None:
+            y_out = torch.empty(rows, self.N, dtype=torch.bfloat16, device=A.device)
+        h, ldh = _mat(h_out, rows, self.N, "h_out")
+        y, ldy = _mat(y_out, rows, self.N, "y_out")
+        r, ldr = _mat(residual, rows, self.N, "residual")
+        g, _ = _mat(gamma.view(1, -1), 1, self.N, "gamma")
+        c, ldc = (0, 0) if partial is None else _mat(partial, self.M, self.N, "partial")
+        parr, ldp = self._peers(peers)
+        _check(lib().entwine_gemm_rs_rmsnorm(self._h, a, lda, b, ldb, parr, ldp, dest, r, ldr, g, float(eps), h, ldh,
+                                             y, ldy, c or None, ldc, ctypes.byref(cfg) if cfg else None,
+                                             _stream_handle(stream)), self._h)
+        return h_out, y_out
 
     def gemm_only(self, A, B, partial=None, cfg: Config | None = None, stream=None):
         import torch
