@@ -12,6 +12,12 @@ events on the producer's stream inside the timed region), the overlap
 efficiency against the uncontended producer (the paper's definition,
 Appendix C) and against GEMM-alone + reduce-alone, and the CPU oracle timed
 on the host on the same workload.
+
+Layer workloads (Section 5.2, layer-level performance) time the call that
+also adds the residual and applies RMSNorm to the reduced chunk, in the same
+launch; their legs compare it with the plain fused call and with the
+unfused chain (sequential GEMM and reduction, then the residual addition and
+RMSNorm as separate device operations).
 """
 from __future__ import annotations
 
@@ -24,6 +30,7 @@ import time
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, published
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E, published
+LAYER_EPS = 1e-5              # RMSNorm epsilon of the layer workloads
 
 
 def parse():
@@ -40,10 +47,13 @@ def parse():
     ap.add_argument("--group-m", type=int, default=None, help="block walk inside a partition (1 = N-major)")
     ap.add_argument("--gemm-wgs", type=int, default=None, help="producer workgroups (persistent grid)")
     ap.add_argument("--launch", type=int, default=None,
-                    help="fused path: 0 = one launch (producer and reducer roles), 1 = two kernels on two streams")
+                    help="fused path: 0 = one launch (producer and reducer roles), 1 = two kernels on two streams, "
+                         "2 = shared CU pool")
+    ap.add_argument("--release-blocks", type=int, default=None,
+                    help="producer blocks per release (-1 = once per workgroup)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-legs", action="store_true", help="skip the gemm-only / reduce-only / sequential legs")
-    ap.add_argument("--only", default=None, choices=["fused", "gemm", "reduce", "seq"],
+    ap.add_argument("--only", default=None, choices=["fused", "gemm", "reduce", "seq", "plain"],
                     help="time just one mode (for profiler runs)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
@@ -116,11 +126,12 @@ def main():
 
     dest_mode = args.dest
     all_chunks = dest_mode == "all"
-    tuned = tuned_config(w.name, "all" if all_chunks else "rank")
+    layer = w.layer
+    tuned = tuned_config(w.name, "layer" if layer else "all" if all_chunks else "rank")
     kw = dict(tuned)
     for k, v in (("order", args.order), ("gemm_cfg", args.gemm_cfg), ("reduce_wgs", args.x),
                  ("reduce_threads", args.b), ("group_m", args.group_m), ("gemm_wgs", args.gemm_wgs),
-                 ("launch", args.launch)):
+                 ("launch", args.launch), ("release_blocks", args.release_blocks)):
         if v is not None:
             kw[k] = v
     cfg = E.Config.make(**kw, record_timing=1)
@@ -138,13 +149,31 @@ def main():
             for d in ([E.DEST_ALL] if all_chunks else range(P))}
     gs = torch.cuda.current_stream()
     rs = torch.cuda.Stream()
+    lay = None
+    if layer:
+        from paper_2609_11562_amd.inputs import make_layer_inputs
+        R_bits, g_bits = make_layer_inputs(ctx.out_rows(dest_of(0)), N)
+        lay = {"R_bits": R_bits, "gamma_bits": g_bits, "R": bits_to_torch(R_bits).cuda(),
+               "gamma": bits_to_torch(g_bits).cuda(), "eps": LAYER_EPS,
+               "h": {d: torch.empty_like(o) for d, o in outs.items()},
+               "y": {d: torch.empty_like(o) for d, o in outs.items()},
+               "h_unfused": {d: torch.empty_like(o) for d, o in outs.items()},
+               "y_unfused": {}}
 
     def step(i, mode="fused"):
         d = dest_of(i)
-        if mode == "fused":
+        if mode == "fused" and layer:
+            ctx.gemm_rs_rmsnorm(A, B, peers, d, lay["R"], lay["gamma"], lay["eps"], h_out=lay["h"][d],
+                                y_out=lay["y"][d], partial=partial, cfg=cfg, stream=gs)
+        elif mode in ("fused", "plain"):
             ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
         elif mode == "seq":
             ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=gs)
+        elif mode == "layer_unfused":
+            # sequential GEMM + reduction, then the epilogue as separate device operations
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=gs)
+            h = torch.add(outs[d], lay["R"], out=lay["h_unfused"][d])
+            lay["y_unfused"][d] = torch.nn.functional.rms_norm(h, (N,), lay["gamma"], lay["eps"])
         elif mode == "gemm":
             ctx.gemm_only(A, B, partial=partial, cfg=cfg, stream=gs)
         else:
@@ -178,16 +207,18 @@ def main():
     # Dominant kernel: the single fused launch (both roles) when the path runs
     # as one kernel, else the producer.  Its mean duration comes from HIP
     # events recorded on the stream it is launched on, inside the timed loop.
-    single = main_mode == "fused" and cfg.launch == 0
+    single = main_mode in ("fused", "plain") and cfg.launch == 0
     mean_k = statistics.fmean(e_ms) if single and e_ms else mean_g
     kernel = "gemm_reduce_fused" if single else "gemm_producer"
     achieved = flops / (mean_k * 1e-3) / 1e12 if mean_k else None
     root = os.path.dirname(os.path.abspath(__file__))
     cfg_now = {"dest": dest_mode, "gemm_cfg": cfg.gemm_cfg, "reduce_wgs": cfg.reduce_wgs, "group_m": cfg.group_m,
-               "launch": cfg.launch}
+               "launch": cfg.launch, "release_blocks": cfg.release_blocks}
     traffic = measured_traffic(root, w.name, kernel, cfg_now) if main_mode == "fused" else None
     rows_out = M if all_chunks else M // P
     algo_bytes = 2.0 * (M * K + K * N + M * N) + 2.0 * rows_out * N * (P + 1)
+    if layer and main_mode == "fused":
+        algo_bytes += 2.0 * rows_out * N * 3     # residual read, h and y written
 
     legs = {}
     if not args.no_legs and args.only is None:
@@ -214,6 +245,28 @@ def main():
             "B_req_GBps": ((P - 1) / P) * M * N * 2 / (med([p[0] for p in p_f]) * 1e-3) / 1e9,
             "gemm_alone_tflops": flops / (T_G * 1e-3) / 1e12,
         }
+        if layer:
+            # T_fused above is the layer call; add the plain fused call and the
+            # unfused chain
+            _, p_p = timed("plain", n_leg, w_leg)
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for i in range(w_leg):
+                step(i, "layer_unfused")
+            ev0.record(gs)
+            for i in range(n_leg):
+                step(i, "layer_unfused")
+            ev1.record(gs)
+            torch.cuda.synchronize()
+            T_layer = T_fused
+            T_plain = med([p[2] for p in p_p])
+            T_unf = ev0.elapsed_time(ev1) / n_leg
+            legs.update({
+                "T_layer_fused_ms": T_layer, "T_gemm_rs_fused_ms": T_plain,
+                "epilogue_cost_ms": T_layer - T_plain,
+                "T_layer_unfused_ms": T_unf,
+                "layer_speedup_vs_unfused": T_unf / T_layer,
+                "eta_layer": T_G / T_layer,
+            })
 
     copy = None
     if args.copy_calib_mib:
@@ -227,7 +280,7 @@ def main():
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(prob, w, outs, all_chunks, dest_of)
+        cpu = cpu_baseline(prob, w, lay["y"] if layer else outs, all_chunks, dest_of, lay)
 
     ctx.close()
     rec = {
@@ -242,12 +295,14 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded bf16 A, B ~ N(0, 0.02); peer partials with matching variance)",
+        "data": "synthetic (seeded bf16 A, B ~ N(0, 0.02); peer partials with matching variance"
+                + ("; residual ~ N(0, 1), gamma ~ U[0.5, 1.5])" if layer else ")"),
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "P": P,
                    "dest": "all" if all_chunks else dest_mode, "mode": main_mode,
                    "order": cfg.order, "gemm_cfg": cfg.gemm_cfg, "reduce_wgs": cfg.reduce_wgs,
                    "reduce_threads": cfg.reduce_threads, "group_m": cfg.group_m, "gemm_wgs": cfg.gemm_wgs,
-                   "launch": cfg.launch},
+                   "launch": cfg.launch, "release_blocks": cfg.release_blocks,
+                   "epilogue": "residual + RMSNorm" if layer else None},
         "roofline": {"bound": "mfma", "kernel": kernel,
                      "achieved": round(achieved, 2) if achieved else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -267,12 +322,15 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(prob, w, outs, all_chunks, dest_of):
+def cpu_baseline(prob, w, outs, all_chunks, dest_of, lay=None):
     """The CPU oracle, as it stands, timed on the host: every chunk of the
-    workload (the whole job), repeated until about 10 s have elapsed or three
-    runs are done.  Also compares the GPU's last outputs on sampled rows."""
+    workload (the whole job; with the layer epilogue, each chunk followed by
+    the residual addition and RMSNorm), repeated until about 10 s have elapsed
+    or three runs are done.  Also compares the GPU's last outputs (y for the
+    layer workloads) on sampled rows of chunk 0."""
     import numpy as np
     import oracle
+    from oracle import layer as L
     try:
         from threadpoolctl import threadpool_info
         threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
@@ -285,7 +343,9 @@ def cpu_baseline(prob, w, outs, all_chunks, dest_of):
         t0 = time.perf_counter()
         C = oracle.local_partial(prob.A, prob.B)
         for d in range(w.P):
-            oracle.reduce_chunk(C, prob.peers, w.P, d)
+            O = oracle.reduce_chunk(C, prob.peers, w.P, d)
+            if lay is not None:
+                L.layer(O, lay["R_bits"], lay["gamma_bits"], lay["eps"])
         runs.append(time.perf_counter() - t0)
         del C
     t = statistics.median(runs)
@@ -295,11 +355,19 @@ def cpu_baseline(prob, w, outs, all_chunks, dest_of):
     rows = np.arange(0, o.shape[0], max(1, o.shape[0] // 16))   # chunk 0 rows are global rows
     ref = oracle.output_rows(prob.A, prob.B, prob.peers, rows)
     got = oracle.bf16_to_f64(o[rows])
-    bound = oracle.error_bound_rows(prob.A, prob.B, prob.peers, rows)
+    if lay is None:
+        bound = oracle.error_bound_rows(prob.A, prob.B, prob.peers, rows)
+    else:
+        R = lay["R_bits"][rows]
+        h, ref = L.layer(ref, R, lay["gamma_bits"], lay["eps"])
+        sb = oracle.error_bound_rows(prob.A, prob.B, prob.peers, rows, final_rounding=False)
+        bound = L.y_bound(h, L.h_bound(sb, h, R), lay["gamma_bits"], lay["eps"])
+    what = "reduce-scatter" + (" + residual addition + RMSNorm" if lay is not None else "")
     return {"value": round(w.flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "seconds_per_job": round(t, 3), "runs": len(runs),
-            "sample": f"whole job ({w.name}, all {w.P} chunks, fp64 numpy), median of {len(runs)} runs",
-            "gpu_spot_check": {"rows": int(len(rows)), "max_abs_err": float(np.abs(got - ref).max()),
+            "sample": f"whole job ({w.name}, all {w.P} chunks, {what}, fp64 numpy), median of {len(runs)} runs",
+            "gpu_spot_check": {"rows": int(len(rows)), "output": "y" if lay is not None else "out",
+                               "max_abs_err": float(np.abs(got - ref).max()),
                                "within_bound": bool(np.all(np.abs(got - ref) <= bound)),
                                "paper_gate": bool(np.all(oracle.paper_gate(got, ref)))}}
 

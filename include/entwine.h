@@ -147,8 +147,6 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
                                void* out, int64_t ldo, void* partial, int64_t ldc,
                                const entwine_config* cfg, void* gemm_stream, void* reduce_stream);
 
-/* Producer alone (flags still published): partial = bf16(A B).  Used for
- * the uncontended GEMM time of the overlap-efficiency metric (Appendix C). */
 /* The fused path followed by the layer epilogue of the paper's layer-level
  * evaluation (Section 5.2: residual addition and RMSNorm after the
  * reduce-scatter), as one launch on `stream` (cfg->launch must be 0, else
@@ -159,11 +157,14 @@ entwine_status entwine_gemm_rs(entwine_ctx* ctx, const void* A, int64_t lda, con
  *   y[i,:] = bf16(h[i,:] * (mean_j h[i,j]^2 + eps)^(-1/2) * gamma)
  *                                        from the stored bf16 h, fp32 math.
  * residual, h_out, y_out: bf16, out_rows x N (leading dimensions ldr, ldh,
- * ldy); gamma: bf16, N; eps > 0 and finite (ENTWINE_EINVAL otherwise).  The
- * row statistics live in context buffers (a pair, used by alternate calls),
- * so calls on one context are ordered by their stream.  h is reproducible
- * bit for bit; y is not (the per-row sums of squares are accumulated with
- * atomics in a varying order).  Errors as entwine_gemm_rs. */
+ * ldy); gamma: bf16, N; eps > 0 and finite (ENTWINE_EINVAL otherwise);
+ * N <= 16384 (a row is held in registers; ENTWINE_EUNSUPPORTED otherwise).
+ * h_out may be the residual itself (same pointer and leading dimension: an
+ * in-place update of the residual stream); otherwise h_out and y_out must
+ * not overlap each other or any input.  Each row is
+ * reduced and normalised by one workgroup once every tile of its tile row
+ * is published, so both h and y are reproducible bit for bit.  Errors as
+ * entwine_gemm_rs. */
 entwine_status entwine_gemm_rs_rmsnorm(entwine_ctx* ctx, const void* A, int64_t lda, const void* B,
                                        int64_t ldb, const void* const* peers, int64_t ldp, int32_t dest,
                                        const void* residual, int64_t ldr, const void* gamma, float eps,
@@ -171,6 +172,8 @@ entwine_status entwine_gemm_rs_rmsnorm(entwine_ctx* ctx, const void* A, int64_t 
                                        void* partial, int64_t ldc, const entwine_config* cfg,
                                        void* stream);
 
+/* Producer alone (flags still published): partial = bf16(A B).  Used for
+ * the uncontended GEMM time of the overlap-efficiency metric (Appendix C). */
 entwine_status entwine_gemm_only(entwine_ctx* ctx, const void* A, int64_t lda, const void* B,
                                  int64_t ldb, void* partial, int64_t ldc,
                                  const entwine_config* cfg, void* stream);

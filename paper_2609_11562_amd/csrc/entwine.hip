@@ -63,9 +63,6 @@ struct entwine_ctx {
   TimingSlot ring[kRing];
   unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, producer end, end}, on first need
   unsigned int* task_ctr = nullptr;       // single launch: {next task, finished workgroups}, zero between calls
-  float* layer_sumsq = nullptr;           // layer epilogue: 2 x M per-row sums of squares (pair by call parity)
-  unsigned int* layer_rows = nullptr;     // layer epilogue: 2 x M/64 row-group counters
-  int64_t layer_calls = 0;
   int64_t ncalls = 0;          // calls with record_timing
   hipStream_t last_stream = nullptr;
   std::string err;
@@ -404,23 +401,15 @@ entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs&
   ra.ntasks = 2 * tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
   ra.ntasks_reduce = ra.ntasks;
   if (layer) {
-    // Reduce tasks, then as many normalise tasks; statistics buffers are a
-    // pair used by alternate layer calls, each call clearing the other.
-    const int64_t rows = dest == ENTWINE_DEST_ALL ? ctx->M : ctx->M / ctx->P;
-    const int par = int(ctx->layer_calls++ & 1);
+    // One task per output row (reducer_layer).
     ra.layer = 1;
-    ra.ntasks = 2 * ra.ntasks_reduce;
+    ra.ntasks = int(dest == ENTWINE_DEST_ALL ? ctx->M : ctx->M / ctx->P);
     ra.residual = static_cast<const uint16_t*>(layer->residual);
     ra.ldr = layer->ldr;
     ra.gamma = static_cast<const uint16_t*>(layer->gamma);
     ra.eps = layer->eps;
     ra.y = static_cast<uint16_t*>(layer->y);
     ra.ldy = layer->ldy;
-    ra.out_rows = rows;
-    ra.sumsq = ctx->layer_sumsq + par * ctx->M;
-    ra.next_sumsq = ctx->layer_sumsq + (1 - par) * ctx->M;
-    ra.rows_done = ctx->layer_rows + par * (ctx->M / 64);
-    ra.next_rows_done = ctx->layer_rows + (1 - par) * (ctx->M / 64);
   }
   const int G = producer_grid(ctx, r, true);
   const int grid = G + r.x;
@@ -555,8 +544,6 @@ entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
   if (ctx->zeros) (void)hipFree(ctx->zeros);
   if (ctx->stamps) (void)hipFree(ctx->stamps);
   if (ctx->task_ctr) (void)hipFree(ctx->task_ctr);
-  if (ctx->layer_sumsq) (void)hipFree(ctx->layer_sumsq);
-  if (ctx->layer_rows) (void)hipFree(ctx->layer_rows);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   for (auto& s : ctx->ring) {
@@ -643,7 +630,7 @@ entwine_status entwine_gemm_rs_rmsnorm(entwine_ctx* ctx, const void* A, int64_t 
   CHECK(resolve(ctx, ctx->M, ctx->N, ctx->P, dest, cfg, ctx->cus, &r));
   if (r.launch != 0) return fail(ctx, ENTWINE_EUNSUPPORTED, "the layer epilogue runs as one launch (launch 0)");
   if (!(eps > 0.0f) || !(eps < 1e30f)) return fail(ctx, ENTWINE_EINVAL, "eps must be positive and finite");
-  const int64_t rows = dest == ENTWINE_DEST_ALL ? ctx->M : ctx->M / ctx->P;
+  if (ctx->N > kLayerMaxN) return fail(ctx, ENTWINE_EUNSUPPORTED, "the layer epilogue holds a row in registers: N <= %d", kLayerMaxN);
   CHECK(check_matrix(ctx, A, lda, ctx->K, "A"));
   CHECK(check_matrix(ctx, B, ldb, ctx->N, "B"));
   CHECK(check_operand_ld(ctx, lda, ldb));
@@ -660,13 +647,6 @@ entwine_status entwine_gemm_rs_rmsnorm(entwine_ctx* ctx, const void* A, int64_t 
     ldc = ctx->N;
   }
   HIP_OR_FAIL(ctx, hipSetDevice(ctx->device));
-  if (!ctx->layer_sumsq) {
-    HIP_OR_FAIL(ctx, hipMalloc(&ctx->layer_sumsq, size_t(2 * ctx->M) * sizeof(float)));
-    HIP_OR_FAIL(ctx, hipMalloc(&ctx->layer_rows, size_t(2 * (ctx->M / 64)) * sizeof(unsigned int)));
-    HIP_OR_FAIL(ctx, hipMemset(ctx->layer_sumsq, 0, size_t(2 * ctx->M) * sizeof(float)));
-    HIP_OR_FAIL(ctx, hipMemset(ctx->layer_rows, 0, size_t(2 * (ctx->M / 64)) * sizeof(unsigned int)));
-  }
-  (void)rows;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint32_t epoch = next_epoch(ctx);
   TimingSlot* ts = timing_slot(ctx, r);

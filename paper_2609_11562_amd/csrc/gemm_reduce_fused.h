@@ -30,24 +30,32 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   const unsigned long long t0 = stamps ? wall_clock64() : 0;
   const int b = blockIdx.x;
   publish_peer_slice(r, np, b, gridDim.x);
-  if (r.layer) {   // clear the other statistics buffers for the next layer call
-    for (int64_t i = int64_t(b) * blockDim.x + threadIdx.x; i < r.out_rows; i += int64_t(gridDim.x) * blockDim.x) {
-      r.next_sumsq[i] = 0.0f;
-      if (i % (kTile / 2) == 0) r.next_rows_done[i / (kTile / 2)] = 0u;
-    }
-  }
   if (b < G) producer_body<BM, BN, TAIL>(g, b, G, smem);
   const unsigned long long t1 = stamps ? wall_clock64() : 0;
   int* s = reinterpret_cast<int*>(smem);
-  switch (np) {
-    case 1: reducer_dynamic<256, 1>(r, s); break;
-    case 2: reducer_dynamic<256, 2>(r, s); break;
-    case 3: reducer_dynamic<256, 3>(r, s); break;
-    case 4: reducer_dynamic<256, 4>(r, s); break;
-    case 5: reducer_dynamic<256, 5>(r, s); break;
-    case 6: reducer_dynamic<256, 6>(r, s); break;
-    case 7: reducer_dynamic<256, 7>(r, s); break;
-    default: reducer_dynamic<256, 8>(r, s); break;
+  static_assert(kLayerThreads == 256, "the layer tasks run on the fused launch's workgroups");
+  if (r.layer) {
+    switch (np) {
+      case 1: reducer_layer<1>(r, s); break;
+      case 2: reducer_layer<2>(r, s); break;
+      case 3: reducer_layer<3>(r, s); break;
+      case 4: reducer_layer<4>(r, s); break;
+      case 5: reducer_layer<5>(r, s); break;
+      case 6: reducer_layer<6>(r, s); break;
+      case 7: reducer_layer<7>(r, s); break;
+      default: reducer_layer<8>(r, s); break;
+    }
+  } else {
+    switch (np) {
+      case 1: reducer_dynamic<256, 1>(r, s); break;
+      case 2: reducer_dynamic<256, 2>(r, s); break;
+      case 3: reducer_dynamic<256, 3>(r, s); break;
+      case 4: reducer_dynamic<256, 4>(r, s); break;
+      case 5: reducer_dynamic<256, 5>(r, s); break;
+      case 6: reducer_dynamic<256, 6>(r, s); break;
+      case 7: reducer_dynamic<256, 7>(r, s); break;
+      default: reducer_dynamic<256, 8>(r, s); break;
+    }
   }
   if (stamps) {
     __syncthreads();

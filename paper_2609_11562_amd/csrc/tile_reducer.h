@@ -45,22 +45,17 @@ struct ReduceArgs {
                            // workgroup's tiles before consuming them
   int withhold_peer;       // with publish_peers: peer left unpublished, or -1
   unsigned int* task_ctr;  // dynamic tasks: {next task, finished workgroups}
-  int ntasks;              // dynamic tasks: all tasks of this call
+  int ntasks;              // dynamic tasks of this call
+  int ntasks_reduce;       // half-tiles the call reduces (their peer flags are published)
   // Layer epilogue (residual addition + RMSNorm after the reduce-scatter):
-  // `out` receives the residual stream h = sum + residual, `y` the
-  // normalised rows; tasks [0, ntasks_reduce) reduce, the rest normalise.
+  // tasks are output rows; `out` receives the residual stream h = sum +
+  // residual and `y` the normalised rows.
   int layer;
-  int ntasks_reduce;
   const uint16_t* residual;  // rows like `out`, leading dimension ldr
   int64_t ldr, ldy;
   const uint16_t* gamma;     // N weights
   uint16_t* y;
   float eps;
-  float* sumsq;              // per output row, zero on entry
-  unsigned int* rows_done;   // per 64 output rows: half-tiles reduced, zero on entry
-  float* next_sumsq;         // the other buffers of the pair, cleared for the next call
-  unsigned int* next_rows_done;
-  int64_t out_rows;
 };
 
 typedef uint32_t r_u32x4_t __attribute__((ext_vector_type(4)));
@@ -139,7 +134,6 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
   for (int v0 = 0; v0 < VPT; v0 += G) {
     r_u32x4_t lv[G];
     r_u32x4_t pv[NP > 1 ? NP - 1 : 1][G];
-    r_u32x4_t rv[G];
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const int v = threadIdx.x + THREADS * (v0 + gi);
@@ -147,7 +141,6 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
       lv[gi] = ld_stream(a.partial + (grow0 + r) * a.ldc + gcol0 + cc);
 #pragma unroll
       for (int q = 0; q < NP - 1; ++q) pv[q][gi] = ld_stream(a.peers[q] + (grow0 + r) * a.ldp + gcol0 + cc);
-      if (a.layer) rv[gi] = ld_stream(a.residual + (orow0 + r) * a.ldr + gcol0 + cc);
     }
     if (v0 == 0) after_first_loads();
 #pragma unroll
@@ -165,65 +158,13 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, int gt, int til
           acc[2 * e] += __builtin_bit_cast(float, pv[q][gi][e] << 16);
           acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][gi][e] & 0xffff0000u);
         }
-      if (a.layer) {   // residual stream: the sum plus the residual, in fp32
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] += __builtin_bit_cast(float, rv[gi][e] << 16);
-          acc[2 * e + 1] += __builtin_bit_cast(float, rv[gi][e] & 0xffff0000u);
-        }
-      }
       r_u32x4_t o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
       const int v = threadIdx.x + THREADS * (v0 + gi);
       const int64_t r = v >> 4, cc = (v & 15) * 8;
       __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc));
-      if (a.layer) {
-        // Sum of squares of the stored (bf16) residual stream for this row:
-        // the 16 lanes holding one row fold their parts, one atomic per row.
-        float ss = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float lo = __builtin_bit_cast(float, o[e] << 16);
-          const float hi = __builtin_bit_cast(float, o[e] & 0xffff0000u);
-          ss += lo * lo + hi * hi;
-        }
-        ss += __shfl_xor(ss, 8, 16);
-        ss += __shfl_xor(ss, 4, 16);
-        ss += __shfl_xor(ss, 2, 16);
-        ss += __shfl_xor(ss, 1, 16);
-        if ((threadIdx.x & 15) == 0) unsafeAtomicAdd(a.sumsq + orow0 + r, ss);
-      }
     }
-  }
-}
-
-// Normalises ROWS rows of tile gt starting at tile row `row0` (layer
-// epilogue): y = bf16(h * (mean of squares + eps)^(-1/2) * gamma), h read
-// back as stored, the mean from the completed per-row sums.
-template <int THREADS, int ROWS>
-__device__ __forceinline__ void normalize_rows(const ReduceArgs& a, int gt, int tiles_n, int row0, int np) {
-  constexpr int VPT = (ROWS * kTile * 2 / 16) / THREADS;
-  const int64_t grow0 = static_cast<int64_t>(gt / tiles_n) * kTile + row0;
-  const int64_t gcol0 = static_cast<int64_t>(gt % tiles_n) * kTile;
-  const int64_t orow0 = a.dest >= 0 ? grow0 - static_cast<int64_t>(a.dest) * (a.M / np) : grow0;
-  const float inv_n = 1.0f / static_cast<float>(a.N);
-#pragma unroll
-  for (int i = 0; i < VPT; ++i) {
-    const int v = threadIdx.x + THREADS * i;
-    const int64_t r = v >> 4, cc = (v & 15) * 8;
-    const float rstd = rsqrtf(a.sumsq[orow0 + r] * inv_n + a.eps);
-    const r_u32x4_t h = *reinterpret_cast<const r_u32x4_t*>(a.out + (orow0 + r) * a.ldo + gcol0 + cc);
-    const r_u32x4_t g = *reinterpret_cast<const r_u32x4_t*>(a.gamma + gcol0 + cc);
-    r_u32x4_t o;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = __builtin_bit_cast(float, h[e] << 16) * rstd * __builtin_bit_cast(float, g[e] << 16);
-      const float hi = __builtin_bit_cast(float, h[e] & 0xffff0000u) * rstd *
-                       __builtin_bit_cast(float, g[e] & 0xffff0000u);
-      o[e] = rnd_pack_bf16x2(lo, hi);
-    }
-    __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.y + (orow0 + r) * a.ldy + gcol0 + cc));
   }
 }
 
@@ -322,7 +263,7 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
   const int ntiles = (a.M / kTile) * tiles_n;
   const int lane = threadIdx.x & 63;
   auto task_tile = [&](int task) {
-    const int u = (task >= a.ntasks_reduce ? task - a.ntasks_reduce : task) >> 1;
+    const int u = task >> 1;
     const int part = a.dest >= 0 ? a.dest : u % NP;
     const int idx = a.dest >= 0 ? u : u / NP;
     int tr, tc;
@@ -337,51 +278,220 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
   while (task < a.ntasks) {
     const int gt = task_tile(task);
     const int row0 = (task & 1) * (kTile / 2);
-    const bool normalise = task >= a.ntasks_reduce;
-    // Layer epilogue: the 64 output rows of this half-tile, counted in
-    // rows_done once reduced in every tile column.
-    const int64_t hrow = (gt / tiles_n) * kTile + row0 - (a.dest >= 0 ? int64_t(a.dest) * (a.M / NP) : 0);
-    unsigned int* const done = a.layer ? a.rows_done + hrow / (kTile / 2) : nullptr;
     if (threadIdx.x < 64) {
       if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
       if (!timed_out) {
-        if (!normalise) {
-          const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
-          timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
-        } else if (lane == 0) {
-          // every tile column of these rows reduced (so their sums are complete)
-          const uint64_t deadline = wall_clock64() + a.timeout_ticks;
-          while (__hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < static_cast<unsigned>(tiles_n)) {
-            if (wall_clock64() > deadline) {
-              if (atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
-                atomicExch(a.status + 1, gt);
-                atomicExch(a.status + 2, -3);   // -3: row statistics incomplete
-              }
-              timed_out = true;
-              break;
-            }
-            __builtin_amdgcn_s_sleep(8);
-          }
-        }
-        timed_out = __shfl(timed_out, 0);
+        const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
+        timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
       }
       if (lane == 0) acquire_fence();
     }
     __syncthreads();
     const int next = s[1];
-    if (!normalise) {
-      reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, row0, [] {});
-      if (a.layer) {
-        __syncthreads();   // every lane's stores and row sums issued
-        if (threadIdx.x == 0) {
-          release_fence();
-          __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, row0, [] {});
+    __syncthreads();   // s[1] is rewritten next
+    task = next;
+  }
+  if (threadIdx.x == 0 && atomicAdd(a.task_ctr + 1, 1u) == gridDim.x - 1) {
+    atomicExch(a.task_ctr, 0u);
+    atomicExch(a.task_ctr + 1, 0u);
+  }
+}
+
+// ------------------------------------------------------------ layer epilogue
+// Residual addition and RMSNorm after the reduce-scatter (paper Section 5.2,
+// layer-level evaluation), as tasks of the same launch.  A task is one output
+// row over all N columns: each of its 256 threads owns 8 columns in every
+// step of 2048, reduces them exactly as ReduceTile does (local contribution,
+// then the peers in rank order, in fp32), adds the residual in fp32, stores
+// the bf16 residual stream h and keeps it in registers.  The row's sum of
+// squares of the stored h is folded across the workgroup through the LDS, and
+// y = bf16(h * (sum / N + eps)^(-1/2) * gamma) is stored next.  A row needs
+// every tile of its tile row, so wave 0 waits for all of their flags; the
+// first poll for the next task's tile row is issued behind the current row's
+// first loads.  A task writes only its own row, which nothing else in the call
+// reads, so it publishes nothing.
+constexpr int kLayerThreads = 256;
+constexpr int kLayerCols = kLayerThreads * 8;   // columns per step
+constexpr int kLayerMaxSteps = 8;
+constexpr int kLayerMaxN = kLayerCols * kLayerMaxSteps;
+
+// Lane `lane` of wave 0: are the NP flags of every tile it checks in tile row
+// tr (columns lane, lane + 64, ...) at the epoch?
+template <int NP>
+__device__ __forceinline__ bool row_flags_ready(const ReduceArgs& a, int tr, int tiles_n, int ntiles) {
+  const int epoch = static_cast<int>(a.epoch);
+  bool ok = true;
+  for (int tc = threadIdx.x & 63; tc < tiles_n; tc += 64) {
+#pragma unroll
+    for (int q = 0; q < NP; ++q) ok &= poll_relaxed(flag_of_lane(a, q, ntiles, tr * tiles_n + tc)) == epoch;
+  }
+  return ok;
+}
+
+// Wave 0: wait until every flag of tile row tr is at the epoch (`ok` is this
+// lane's first poll).  On timeout records the first missing flag's tile and
+// source (-1 local, q peer q) and returns false.
+template <int NP>
+__device__ __forceinline__ bool wave_await_row(const ReduceArgs& a, int tr, int tiles_n, int ntiles, bool ok) {
+  const int epoch = static_cast<int>(a.epoch);
+  const uint64_t deadline = wall_clock64() + a.timeout_ticks;
+  while (__ballot(!ok) != 0) {
+    if (wall_clock64() > deadline) {
+      if ((threadIdx.x & 63) == __builtin_ctzll(__ballot(!ok))) {
+        int tile = tr * tiles_n, src = -1;   // this lane's first missing flag
+        for (int tc = threadIdx.x & 63, found = 0; tc < tiles_n && !found; tc += 64)
+          for (int q = 0; q < NP && !found; ++q)
+            if (poll_relaxed(flag_of_lane(a, q, ntiles, tr * tiles_n + tc)) != epoch) {
+              tile = tr * tiles_n + tc;
+              src = q - 1;
+              found = 1;
+            }
+        if (atomicCAS(a.status, 0, ENTWINE_ETIMEOUT) == 0) {
+          atomicExch(a.status + 1, tile);
+          atomicExch(a.status + 2, src);
         }
       }
-    } else {
-      normalize_rows<THREADS, kTile / 2>(a, gt, tiles_n, row0, NP);
+      return false;
     }
-    __syncthreads();   // s[1] is rewritten next
+    __builtin_amdgcn_s_sleep(8);
+    if (!ok) ok = row_flags_ready<NP>(a, tr, tiles_n, ntiles);
+  }
+  return true;
+}
+
+// Output row `orow` of the call (a row of `out`): h, its sum of squares, y.
+// `red` is kLayerThreads / 64 floats of LDS.
+template <int NP, typename Hook>
+__device__ __forceinline__ void layer_row(const ReduceArgs& a, int64_t orow, float* red, Hook after_first_loads) {
+  constexpr int B = 4;   // steps per batch: (NP + 1) x 4 loads in flight per lane
+  static_assert(kLayerMaxSteps % B == 0, "batches tile the steps");
+  const int64_t grow = orow + (a.dest >= 0 ? static_cast<int64_t>(a.dest) * (a.M / NP) : 0);
+  const int c0 = threadIdx.x * 8;
+  const int steps = (a.N + kLayerCols - 1) / kLayerCols;
+  r_u32x4_t h[kLayerMaxSteps];
+  float ss = 0.0f;
+#pragma unroll
+  for (int s0 = 0; s0 < kLayerMaxSteps; s0 += B) {
+    if (s0 >= steps) break;
+    r_u32x4_t lv[B], rv[B];
+    r_u32x4_t pv[NP > 1 ? NP - 1 : 1][B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int c = (s0 + b) * kLayerCols + c0;
+      if (c < a.N) {
+        lv[b] = ld_stream(a.partial + grow * a.ldc + c);
+#pragma unroll
+        for (int q = 0; q < NP - 1; ++q) pv[q][b] = ld_stream(a.peers[q] + grow * a.ldp + c);
+        rv[b] = ld_stream(a.residual + orow * a.ldr + c);
+      }
+    }
+    if (s0 == 0) after_first_loads();
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int c = (s0 + b) * kLayerCols + c0;
+      h[s0 + b] = r_u32x4_t{0u, 0u, 0u, 0u};
+      if (c >= a.N) continue;
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = __builtin_bit_cast(float, lv[b][e] << 16);
+        acc[2 * e + 1] = __builtin_bit_cast(float, lv[b][e] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __builtin_bit_cast(float, pv[q][b][e] << 16);
+          acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][b][e] & 0xffff0000u);
+        }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += __builtin_bit_cast(float, rv[b][e] << 16);
+        acc[2 * e + 1] += __builtin_bit_cast(float, rv[b][e] & 0xffff0000u);
+      }
+      r_u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+        const float lo = __builtin_bit_cast(float, o[e] << 16);
+        const float hi = __builtin_bit_cast(float, o[e] & 0xffff0000u);
+        ss += lo * lo + hi * hi;
+      }
+      h[s0 + b] = o;
+      __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + orow * a.ldo + c));
+    }
+  }
+  // gamma for every step, issued before the row sum's barrier
+  r_u32x4_t g[kLayerMaxSteps];
+#pragma unroll
+  for (int st = 0; st < kLayerMaxSteps; ++st) {
+    const int c = st * kLayerCols + c0;
+    if (st < steps && c < a.N) g[st] = *reinterpret_cast<const r_u32x4_t*>(a.gamma + c);
+  }
+  ss += __shfl_xor(ss, 32);
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 8);
+  ss += __shfl_xor(ss, 4);
+  ss += __shfl_xor(ss, 2);
+  ss += __shfl_xor(ss, 1);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  static_assert(kLayerThreads == 256, "four wave sums");
+  const float rstd = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) * (1.0f / static_cast<float>(a.N)) + a.eps);
+#pragma unroll
+  for (int st = 0; st < kLayerMaxSteps; ++st) {
+    const int c = st * kLayerCols + c0;
+    if (st >= steps || c >= a.N) continue;
+    r_u32x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __builtin_bit_cast(float, h[st][e] << 16) * rstd * __builtin_bit_cast(float, g[st][e] << 16);
+      const float hi = __builtin_bit_cast(float, h[st][e] & 0xffff0000u) * rstd *
+                       __builtin_bit_cast(float, g[st][e] & 0xffff0000u);
+      o[e] = rnd_pack_bf16x2(lo, hi);
+    }
+    __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.y + orow * a.ldy + c));
+  }
+}
+
+// The layer epilogue's task loop (blockDim.x == kLayerThreads): output rows
+// taken from the device counter in order, each once all tiles of its tile
+// row are published; counters returned to zero as in reducer_dynamic.
+// s: eight ints of LDS.
+template <int NP>
+__device__ __forceinline__ void reducer_layer(const ReduceArgs& a, int* s) {
+  const int tiles_n = a.N / kTile;
+  const int ntiles = (a.M / kTile) * tiles_n;
+  const int64_t first_row = a.dest >= 0 ? static_cast<int64_t>(a.dest) * (a.M / NP) : 0;
+  auto tile_row = [&](int task) { return static_cast<int>((first_row + task) / kTile); };
+  float* red = reinterpret_cast<float*>(s + 4);
+  __syncthreads();   // producer waves are done with the LDS
+  if (threadIdx.x == 0) s[0] = static_cast<int>(atomicAdd(a.task_ctr, 1u));
+  __syncthreads();
+  int task = s[0];
+  bool timed_out = false;              // wave 0
+  bool have_poll = false, polled = false;   // wave 0: a poll of this task's tile row made early
+  while (task < a.ntasks) {
+    const int tr = tile_row(task);
+    if (threadIdx.x < 64) {
+      if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
+      if (!timed_out) {
+        const bool ok = have_poll ? polled : row_flags_ready<NP>(a, tr, tiles_n, ntiles);
+        timed_out = !wave_await_row<NP>(a, tr, tiles_n, ntiles, ok);
+      }
+      if ((threadIdx.x & 63) == 0) acquire_fence();
+    }
+    __syncthreads();
+    const int next = s[1];
+    have_poll = false;
+    layer_row<NP>(a, task, red, [&] {
+      if (threadIdx.x < 64 && next < a.ntasks && !timed_out) {
+        polled = row_flags_ready<NP>(a, tile_row(next), tiles_n, ntiles);
+        have_poll = true;
+      }
+    });
+    __syncthreads();   // s[1] and the row sums are rewritten next
     task = next;
   }
   if (threadIdx.x == 0 && atomicAdd(a.task_ctr + 1, 1u) == gridDim.x - 1) {

@@ -10,6 +10,8 @@ Every array is returned as raw bfloat16 bit patterns (``numpy.uint16``):
 * ``B``      K x N, row-major (N contiguous)
 * ``peers``  P-1 arrays of M x N, row-major; peer ``q`` stands for the q-th
              rank other than the local one, in ascending rank order.
+* layer epilogue (``make_layer_inputs``): the residual stream, rows x N
+  row-major, and the RMSNorm weight gamma, length N.
 
 Draws come from numpy's PCG64 generator: A from ``seed``, B from ``seed + 1``
 and peer ``q`` from ``seed + 2 + q``.  Values are drawn in float32 and rounded
@@ -78,6 +80,16 @@ def make_problem(M: int, N: int, K: int, P: int, ab: Dist, peer: Dist,
     B = draw_bf16(seed + 1, (K, N), ab)
     peers = [draw_bf16(seed + 2 + q, (M, N), peer) for q in range(P - 1)]
     return Problem(M, N, K, P, A, B, peers)
+
+
+def make_layer_inputs(rows: int, N: int, seed: int = BASE_SEED, residual: Dist = Dist("normal", 1.0)):
+    """(R, gamma) for the residual addition + RMSNorm after the reduce-scatter:
+    R ~ ``residual`` (hidden states of order one by default) from
+    ``seed + 100``, gamma ~ U[0.5, 1.5] from ``seed + 101``."""
+    R = draw_bf16(seed + 100, (rows, N), residual)
+    rng = np.random.Generator(np.random.PCG64(seed + 101))
+    gamma = to_bf16_bits(rng.uniform(0.5, 1.5, size=N).astype(np.float32))
+    return R, gamma
 
 
 def bits_to_torch(bits: np.ndarray) -> torch.Tensor:

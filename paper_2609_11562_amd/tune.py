@@ -5,7 +5,9 @@ count b by the lowest end-to-end latency under concurrent execution, with an
 offline profiler (Section 3.2 "End-to-end optimization", Section 4.3).  This
 module does the same on the device it runs on: for one workload it times the
 fused call over a grid of (block shape, x, b, block walk) and records the
-winner in ``tuned.json`` (read back by :func:`tuning.tuned_config`).
+winner in ``tuned.json`` (read back by :func:`tuning.tuned_config`).  The
+"layer" scope times the call with the residual addition and RMSNorm
+(Section 5.2, layer-level performance), which runs as one launch only.
 
 Timing follows the benchmark: synthetic seeded inputs resident on the device,
 ``warmup`` untimed calls, then ``steps`` calls whose wall time (host clock
@@ -37,12 +39,16 @@ DEFAULT_CFGS = (E.GEMM_256x256, E.GEMM_256x128, E.GEMM_128x256, E.GEMM_128x128)
 DEFAULT_GROUP_M = (1, 4)
 
 
-def _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs):
+def _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs, layer=None):
     import torch
 
     def call(i):
         d = E.DEST_ALL if scope == "all" else i % P
-        ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
+        if scope == "layer":
+            R, gamma, h, y = layer
+            ctx.gemm_rs_rmsnorm(A, B, peers, d, R, gamma, 1e-5, h_out=h, y_out=y, partial=partial, cfg=cfg, stream=gs)
+        else:
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
 
     for i in range(warmup):
         call(i)
@@ -68,6 +74,8 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
     only its first value is tried."""
     import torch
 
+    if scope == "layer" and launch != 0:
+        raise ValueError("the layer epilogue runs as one launch (launch 0)")
     w = WORKLOADS[workload]
     M, N, K, P = w.M, w.N, w.K, w.P
     prob = w.problem()
@@ -79,6 +87,12 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
         partial = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
         dests = [E.DEST_ALL] if scope == "all" else list(range(P))
         outs = {d: torch.empty(ctx.out_rows(d), N, dtype=torch.bfloat16, device="cuda") for d in dests}
+        layer = None
+        if scope == "layer":
+            R, gamma = w.layer_inputs()
+            layer = (bits_to_torch(R).cuda(), bits_to_torch(gamma).cuda(),
+                     torch.empty(M // P, N, dtype=torch.bfloat16, device="cuda"),
+                     torch.empty(M // P, N, dtype=torch.bfloat16, device="cuda"))
         gs = torch.cuda.current_stream()
         rs = torch.cuda.Stream()
         grid = list(itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms, release_blocks))
@@ -89,7 +103,7 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
                 cfg = E.Config.make(**kw)
                 if E.validate(M, N, K, P, E.DEST_ALL if scope == "all" else 0, cfg) != E.OK:
                     continue   # e.g. a block that does not divide the chunk, or x = -1 with two streams
-                wall, e2e = _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs)
+                wall, e2e = _time_config(ctx, A, B, peers, partial, outs, P, scope, cfg, steps, warmup, gs, rs, layer)
                 row = {k: v for k, v in kw.items() if k != "record_timing"}
                 row.update(order=E.ORDER_INTERLEAVED, wall_ms=round(wall, 5), event_ms=round(e2e, 5),
                            tflops=round(2.0 * M * N * K / (wall * 1e-3) / 1e12, 1))
@@ -118,7 +132,8 @@ def write_entry(workload: str, scope: str, best: dict, path: str = _TABLE) -> No
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--workload", action="append", required=True)
-    ap.add_argument("--scope", default="rank", choices=["rank", "all"])
+    ap.add_argument("--scope", default="rank", choices=["rank", "all", "layer"],
+                    help="rank = one chunk, all = every chunk, layer = one chunk + residual addition + RMSNorm")
     ap.add_argument("--xs", default=",".join(map(str, DEFAULT_XS)))
     ap.add_argument("--bs", default=",".join(map(str, DEFAULT_BS)))
     ap.add_argument("--cfgs", default=",".join(map(str, DEFAULT_CFGS)))

@@ -4,8 +4,9 @@ The paper selects the GEMM block shape, the reducer grid size x and its
 thread count b together, by the lowest end-to-end latency under concurrent
 execution (Section 3.2 "End-to-end optimization", Section 4.3).  The table
 in ``tuned.json`` holds the winners of that sweep, keyed by workload name and
-reduction scope ("rank" = one chunk, "all" = every chunk); anything missing
-falls back to the library defaults.
+scope ("rank" = one chunk, "all" = every chunk, "layer" = one chunk followed
+by the residual addition and RMSNorm); anything missing falls back to the
+library defaults.
 """
 from __future__ import annotations
 

@@ -12,7 +12,7 @@ from __future__ import annotations
 import dataclasses
 import math
 
-from .inputs import BASE_SEED, Dist, Problem, make_problem
+from .inputs import BASE_SEED, Dist, Problem, make_layer_inputs, make_problem
 
 
 @dataclasses.dataclass(frozen=True)
@@ -25,6 +25,7 @@ class Workload:
     ab: Dist
     peer: Dist
     note: str = ""
+    layer: bool = False   # the call adds the residual and applies RMSNorm
 
     @property
     def flops(self) -> float:
@@ -33,10 +34,14 @@ class Workload:
     def problem(self, seed: int = BASE_SEED) -> Problem:
         return make_problem(self.M, self.N, self.K, self.P, self.ab, self.peer, seed)
 
+    def layer_inputs(self, seed: int = BASE_SEED):
+        """(R, gamma) of the layer epilogue for one rank's chunk of M/P rows."""
+        return make_layer_inputs(self.M // self.P, self.N, seed)
 
-def _llm(name, M, K, N, P, note):
+
+def _llm(name, M, K, N, P, note, layer=False):
     s = 0.02
-    return Workload(name, M, N, K, P, Dist("normal", s), Dist("normal", s * s * math.sqrt(K)), note)
+    return Workload(name, M, N, K, P, Dist("normal", s), Dist("normal", s * s * math.sqrt(K)), note, layer)
 
 
 WORKLOADS = {
@@ -61,6 +66,14 @@ for _K in (512, 2048):
         _w = _llm(f"sweep_8192x{_K}x8192_p{_P}", 8192, _K, 8192, _P,
                   "budget / tile-order sweep window (the paper's two K windows)")
         WORKLOADS[_w.name] = _w
+
+# Layer level: the Llama-3-70B attention output projection followed by the
+# residual addition and RMSNorm, at global sequence lengths 4K, 8K and 16K
+# (the GEMM's M; model width and K_local fixed).
+for _S in (4, 8, 16):
+    _w = _llm(f"llama70b_attn_out_layer_seq{_S}k_tp8", _S * 1024, 1024, 8192, 8,
+              f"attention output + residual addition + RMSNorm, {_S}K tokens", layer=True)
+    WORKLOADS[_w.name] = _w
 
 BENCH_WORKLOAD = "llama7b_mlp_down_tp8"
 SMALL_WORKLOAD = "tiny_512x256x1024_p2"

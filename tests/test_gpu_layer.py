@@ -4,7 +4,8 @@ against the float64 oracle.
 
 h (the new residual stream) must match the reducer's own fp32 arithmetic bit
 for bit on the partial of the same call, and both h and y must pass the
-paper's gate and the elementwise rounding bounds of the fused path."""
+paper's gate and the elementwise rounding bounds of the fused path.  Both are
+reproducible bit for bit across configurations (one workgroup per row)."""
 import numpy as np
 import pytest
 import torch
@@ -12,7 +13,8 @@ import torch
 import oracle
 from oracle import layer as L
 from paper_2609_11562_amd import entwine as E
-from paper_2609_11562_amd.inputs import Dist, bits_to_torch, draw_bf16, make_problem, to_bf16_bits
+from paper_2609_11562_amd.inputs import Dist, bits_to_torch, make_layer_inputs, make_problem
+from paper_2609_11562_amd.tuning import tuned_config
 from paper_2609_11562_amd.workloads import WORKLOADS
 
 pytestmark = pytest.mark.gpu
@@ -33,10 +35,7 @@ def out_rows(M, P, dest):
 
 
 def layer_inputs(M, N, P, dest, seed):
-    rows = len(out_rows(M, P, dest))
-    R = draw_bf16(seed, (rows, N), Dist("normal", 1.0))
-    gamma = to_bf16_bits(np.random.default_rng(seed + 1).uniform(0.5, 1.5, N).astype(np.float32))
-    return R, gamma
+    return make_layer_inputs(len(out_rows(M, P, dest)), N, seed)
 
 
 def check_layer(prob, R_bits, gamma, h_bits, y_bits, grow, lrow):
@@ -55,10 +54,12 @@ def check_layer(prob, R_bits, gamma, h_bits, y_bits, grow, lrow):
         assert not bad.any(), f"{name}: bound exceeded at {np.argwhere(bad)[:5].tolist()}"
 
 
-@pytest.mark.parametrize("dest", [1, E.DEST_ALL])
-def test_layer_matches_oracle_and_reducer_arithmetic(dest):
-    M, N, K, P = 1024, 1024, 256, 4
-    print(f"[layer small dest={dest}]", flush=True)
+@pytest.mark.parametrize("dest,N", [(1, 1024), (E.DEST_ALL, 1024), (2, 3200)])
+def test_layer_matches_oracle_and_reducer_arithmetic(dest, N):
+    """N = 3200 leaves a ragged last step of columns (a row is walked 2048
+    columns at a time)."""
+    M, K, P = 1024, 256, 4
+    print(f"[layer small dest={dest} N={N}]", flush=True)
     prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.02), seed=31)
     A, B, peers = dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
     R, gamma = layer_inputs(M, N, P, dest, 40)
@@ -75,10 +76,9 @@ def test_layer_matches_oracle_and_reducer_arithmetic(dest):
 
 
 def test_layer_invariant_across_configs_and_repeated_calls():
-    """h is bitwise stable across block shapes, walks, budgets and repeated
-    calls (which alternate the statistics buffers, with plain fused calls in
-    between); y stays within its bound every time.  Outputs are NaN-poisoned
-    before each call."""
+    """h and y are bitwise stable across block shapes, walks, budgets and
+    repeated calls (with plain fused calls in between), and within their
+    bounds.  Outputs are NaN-poisoned before each call."""
     M, N, K, P = 1024, 2048, 392, 8
     dest = 5
     print("[layer invariants]", flush=True)
@@ -104,30 +104,75 @@ def test_layer_invariant_across_configs_and_repeated_calls():
             assert ctx.query_status()[0] == E.OK
             hb, yb = host_bits(h), host_bits(y)
             if base is None:
-                base = hb
+                base = hb, yb
                 check_layer(prob, R, gamma, hb, yb, grow, np.arange(rows))
             else:
-                assert np.array_equal(hb, base), kw
-                check_layer(prob, R, gamma, hb, yb, grow[::7], np.arange(rows)[::7])
+                assert np.array_equal(hb, base[0]) and np.array_equal(yb, base[1]), kw
             if i % 2 == 0:   # a plain fused call between layer calls
                 ctx.gemm_rs(A, B, peers, i % P, reduce_stream=rs)
                 assert ctx.query_status()[0] == E.OK
 
 
-def test_layer_full_size_attention_output_sampled_rows():
-    w = WORKLOADS["llama70b_attn_out_tp8"]
-    dest = 3
-    print(f"[layer full {w.name} dest={dest}]", flush=True)
+@pytest.mark.parametrize("name", ["llama70b_attn_out_layer_seq4k_tp8", "llama70b_attn_out_layer_seq8k_tp8",
+                                  "llama70b_attn_out_layer_seq16k_tp8"])
+def test_layer_full_size_sampled_rows(name):
+    """Every layer workload at full size, in the launch configuration the
+    benchmark times (its tuned entry) and with a fixed reducer budget, on
+    sampled rows of the first and last chunks."""
+    w = WORKLOADS[name]
     prob = w.problem()
     A, B, peers = dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
-    R, gamma = layer_inputs(w.M, w.N, w.P, dest, 60)
+    R, gamma = w.layer_inputs()
+    Rd, gd = dev(R), dev(gamma)
+    rows = w.M // w.P
+    lrow = np.unique(np.array([0, 1, 63, 64, 127, 128, rows // 2, rows - 65, rows - 1]))
     with E.Context(w.M, w.N, w.K, w.P) as ctx:
+        for dest in (0, w.P - 1):
+            for kw in (tuned_config(name, "layer"), dict(reduce_wgs=16)):
+                print(f"[layer full {name} dest={dest} cfg={kw}]", flush=True)
+                h, y = ctx.gemm_rs_rmsnorm(A, B, peers, dest, Rd, gd, EPS, cfg=E.Config.make(**kw))
+                assert ctx.query_status()[0] == E.OK
+                sel = torch.as_tensor(lrow, device="cuda")
+                hb, yb = host_bits(h[sel]), host_bits(y[sel])
+                grow = out_rows(w.M, w.P, dest)[lrow]
+                check_layer(prob, R[lrow], gamma, hb, yb, grow, np.arange(len(lrow)))
+    del A, B, peers
+    torch.cuda.empty_cache()
+
+
+def test_layer_in_place_residual_update():
+    """h_out may be the residual buffer itself."""
+    M, N, K, P = 1024, 2048, 128, 4
+    dest = 3
+    print("[layer in place]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.02), seed=34)
+    A, B, peers = dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
+    R, gamma = layer_inputs(M, N, P, dest, 80)
+    with E.Context(M, N, K, P) as ctx:
         h, y = ctx.gemm_rs_rmsnorm(A, B, peers, dest, dev(R), dev(gamma), EPS)
+        Rd = dev(R)
+        h2, y2 = ctx.gemm_rs_rmsnorm(A, B, peers, dest, Rd, dev(gamma), EPS, h_out=Rd)
+        assert ctx.query_status()[0] == E.OK and h2.data_ptr() == Rd.data_ptr()
+        assert torch.equal(h.view(torch.int16), h2.view(torch.int16))
+        assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+def test_layer_withheld_peer_times_out_then_recovers():
+    M, N, K, P = 1024, 1024, 128, 4
+    dest = 0
+    print("[layer timeout]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.02), seed=35)
+    A, B, peers = dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
+    R, gamma = layer_inputs(M, N, P, dest, 90)
+    Rd, gd = dev(R), dev(gamma)
+    with E.Context(M, N, K, P) as ctx:
+        ctx.gemm_rs_rmsnorm(A, B, peers, dest, Rd, gd, EPS, cfg=E.Config.make(withhold_peer=1, timeout_us=20000))
+        st, tile, src = ctx.query_status()
+        assert st == E.ETIMEOUT and src == 1 and 0 <= tile < (M // 128) * (N // 128)
+        h, y = ctx.gemm_rs_rmsnorm(A, B, peers, dest, Rd, gd, EPS)
         assert ctx.query_status()[0] == E.OK
-        hb, yb = host_bits(h), host_bits(y)
-    lrow = np.array([0, 1, 63, 64, 127, 128, 511, 700, 1023])
-    grow = out_rows(w.M, w.P, dest)[lrow]
-    check_layer(prob, R, gamma, hb, yb, grow, lrow)
+        grow = out_rows(M, P, dest)
+        check_layer(prob, R, gamma, host_bits(h), host_bits(y), grow, np.arange(len(grow)))
 
 
 def test_layer_rejects_bad_arguments():
@@ -141,4 +186,15 @@ def test_layer_rejects_bad_arguments():
         assert ei.value.status == E.EINVAL
         with pytest.raises(E.EntwineError) as ei:
             ctx.gemm_rs_rmsnorm(A, B, peers, 0, dev(R), dev(gamma), EPS, cfg=E.Config.make(launch=1))
+        assert ei.value.status == E.EUNSUPPORTED
+    # a row wider than the registers that hold it
+    M, N, K, P = 256, 16384 + 128, 64, 2
+    A = torch.zeros(M, K, dtype=torch.bfloat16, device="cuda")
+    B = torch.zeros(K, N, dtype=torch.bfloat16, device="cuda")
+    peer = torch.zeros(M, N, dtype=torch.bfloat16, device="cuda")
+    R = torch.zeros(M // P, N, dtype=torch.bfloat16, device="cuda")
+    gamma = torch.ones(N, dtype=torch.bfloat16, device="cuda")
+    with E.Context(M, N, K, P) as ctx:
+        with pytest.raises(E.EntwineError) as ei:
+            ctx.gemm_rs_rmsnorm(A, B, [peer], 0, R, gamma, EPS)
         assert ei.value.status == E.EUNSUPPORTED

@@ -14,7 +14,8 @@ def test_table_entries_are_valid_configs():
         assert name in WORKLOADS, name
         w = WORKLOADS[name]
         for scope, entry in scopes.items():
-            assert scope in ("rank", "all")
+            assert scope in ("rank", "all", "layer")
+            assert (scope == "layer") == w.layer, (name, scope)
             kw = tuning.tuned_config(name, scope)
             assert set(kw) <= set(tuning._FIELDS) and kw
             dest = E.DEST_ALL if scope == "all" else 0
