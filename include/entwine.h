@@ -111,7 +111,11 @@ typedef struct {
                              tiles after every g of its blocks, one release
                              fence each time (Section 5.3.2, release
                              granularity); 0 = default = 1; -1 = only once,
-                             after its last block */
+                             after its last block; release groups, where a
+                             tile's flag waits for its whole group:
+                             -2 = its row partition (chunk), -3 = the whole
+                             output (the coarse end of Section 5.3.2's
+                             ablation) */
   int32_t store_mode;     /* partial tile stores: 0 = write-through (the
                              release has little dirty data to write back),
                              1 = non-temporal (written back by the release) */

@@ -63,6 +63,7 @@ struct entwine_ctx {
   TimingSlot ring[kRing];
   unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, producer end, end}, on first need
   unsigned int* task_ctr = nullptr;       // single launch: {next task, finished workgroups}, zero between calls
+  unsigned long long* group_ctr = nullptr;  // release groups: tiles stored per partition (P) and output (1)
   int64_t ncalls = 0;          // calls with record_timing
   hipStream_t last_stream = nullptr;
   std::string err;
@@ -135,7 +136,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.group_m < 0 || c.group_m > 64) return fail(ctx, ENTWINE_EINVAL, "group_m outside [0, 64]");
   if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
   if (c.launch < 0 || c.launch > 2) return fail(ctx, ENTWINE_EINVAL, "launch must be 0, 1 or 2");
-  if (c.release_blocks < -1) return fail(ctx, ENTWINE_EINVAL, "release_blocks must be >= -1");
+  if (c.release_blocks < -3) return fail(ctx, ENTWINE_EINVAL, "release_blocks must be >= -3");
   if (c.store_mode < 0 || c.store_mode > 1) return fail(ctx, ENTWINE_EINVAL, "store_mode must be 0 or 1");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
@@ -165,7 +166,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->group_m = c.group_m ? c.group_m : 4;
   r->gemm_wgs = c.gemm_wgs;
   r->launch = c.launch;
-  r->release_blocks = c.release_blocks == 0 ? 1 : c.release_blocks;   // -1 (or any g < 1): at the end
+  r->release_blocks = c.release_blocks == 0 ? 1 : c.release_blocks;   // -1: at the end; -2, -3: groups
   r->store_mode = c.store_mode;
   return ENTWINE_OK;
 }
@@ -294,6 +295,7 @@ GemmArgs gemm_args(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t l
   g.epoch = epoch;
   g.release_blocks = r.release_blocks;
   g.nt_stores = r.store_mode;
+  g.group_ctr = ctx->group_ctr;
   return g;
 }
 
@@ -514,12 +516,14 @@ entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, 
   if (hipMalloc(&c->flags, fbytes) != hipSuccess ||
       hipMalloc(&c->peer_flags, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
       hipMalloc(&c->status, 4 * sizeof(int)) != hipSuccess || hipMalloc(&c->zeros, 256) != hipSuccess ||
-      hipMalloc(&c->task_ctr, 2 * sizeof(unsigned int)) != hipSuccess)
+      hipMalloc(&c->task_ctr, 2 * sizeof(unsigned int)) != hipSuccess ||
+      hipMalloc(&c->group_ctr, size_t(P + 1) * sizeof(unsigned long long)) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_ENOMEM, "flag allocation failed"));
   if (hipMemset(c->flags, 0, fbytes) != hipSuccess ||
       hipMemset(c->peer_flags, 0, fbytes * size_t(P > 1 ? P - 1 : 1)) != hipSuccess ||
       hipMemset(c->status, 0, 4 * sizeof(int)) != hipSuccess || hipMemset(c->zeros, 0, 256) != hipSuccess ||
-      hipMemset(c->task_ctr, 0, 2 * sizeof(unsigned int)) != hipSuccess)
+      hipMemset(c->task_ctr, 0, 2 * sizeof(unsigned int)) != hipSuccess ||
+      hipMemset(c->group_ctr, 0, size_t(P + 1) * sizeof(unsigned long long)) != hipSuccess)
     return bail(fail(nullptr, ENTWINE_EHIP, "flag initialisation failed"));
   if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
@@ -544,6 +548,7 @@ entwine_status entwine_ctx_destroy(entwine_ctx* ctx) {
   if (ctx->zeros) (void)hipFree(ctx->zeros);
   if (ctx->stamps) (void)hipFree(ctx->stamps);
   if (ctx->task_ctr) (void)hipFree(ctx->task_ctr);
+  if (ctx->group_ctr) (void)hipFree(ctx->group_ctr);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   for (auto& s : ctx->ring) {

@@ -76,9 +76,15 @@ struct GemmArgs {
   int M, N, K, P, order, group_m;
   int* flags;             // one per global 128 x 128 tile, row-major; null = no publish
   uint32_t epoch;
-  int release_blocks;     // publish after every g blocks (g >= 1), or only after the last (g <= 0)
+  int release_blocks;     // publish after every g blocks (g >= 1), only after the last (g = -1), or
+                          // by group: -2 a partition's tiles once all are stored, -3 the whole output's
   int nt_stores;          // 1: non-temporal tile stores (written back at the release); 0: write-through
+  unsigned long long* group_ctr;   // release groups: tiles stored, per partition (P) then the output (1);
+                                   // a multiple of the group's tile count between calls
 };
+
+constexpr int kReleasePartition = -2;
+constexpr int kReleaseOutput = -3;
 
 template <int BM_, int BN_>
 struct GemmShape {
@@ -498,15 +504,48 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
       wave_sync();                               // the next round rewrites these rows
     }
 
-    // Release granularity (paper Section 5.3.2): one fence covers the tiles
-    // of every block since the last publication.
-    const bool release = a.flags != nullptr &&
-                         (lb + 1 == mine || (a.release_blocks >= 1 && lb + 1 - unpublished >= a.release_blocks));
-    if (release) {
+    // Release granularity (paper Section 5.3.2): one release covers the
+    // tiles of every block since the last publication.  With release groups
+    // every block is released into its group's counter, and the workgroup
+    // whose block completes the group publishes the group's flags.
+    //
+    // A release starts with every wave waiting for its own tile stores: they
+    // are inline asm, hidden from the compiler's wait tracking, so neither
+    // the barrier nor a fence in another wave waits for them.  Write-through
+    // stores are then in memory, where every XCD's acquire finds them, and
+    // the flags can follow at once; non-temporal stores may still sit dirty
+    // in this XCD's L2 and need the fence's write-back first.
+    const bool grouped = a.release_blocks <= kReleasePartition;
+    const bool release = a.flags != nullptr && (grouped || lb + 1 == mine ||
+                                                (a.release_blocks >= 1 && lb + 1 - unpublished >= a.release_blocks));
+    if (release && grouped) {
+      const int tiles_n = a.N / kTile;
+      const int part_rows = a.M / a.P;
+      const int d = a.release_blocks == kReleasePartition ? bp.mb * BM / part_rows : 0;
+      const int64_t first = a.release_blocks == kReleasePartition ? static_cast<int64_t>(d) * (part_rows / kTile) * tiles_n : 0;
+      const int64_t count = static_cast<int64_t>(a.release_blocks == kReleasePartition ? part_rows : a.M) / kTile * tiles_n;
+      int* const s_last = reinterpret_cast<int*>(smem + NS * S::STAGE);   // wave 0's staging rows, free here
+      wait_vm<0>();
+      __syncthreads();
+      if (tid == 0) {
+        if (a.nt_stores) release_fence();
+        constexpr unsigned long long c = (BM / kTile) * (BN / kTile);
+        unsigned long long* ctr = a.group_ctr + (a.release_blocks == kReleasePartition ? d : a.P);
+        const unsigned long long old = atomicAdd(ctr, c);
+        // every block of the group was released before it was counted
+        *s_last = (old + c) % static_cast<unsigned long long>(count) == 0;
+      }
+      __syncthreads();
+      if (*s_last)
+        for (int64_t i = tid; i < count; i += 256) publish_relaxed(a.flags + first + i, a.epoch);
+      __syncthreads();   // s_last lives in staging rows the next epilogue rewrites
+      unpublished = lb + 1;
+    } else if (release) {
+      wait_vm<0>();
       __syncthreads();
       if (tid == 0) {
         const int tiles_n = a.N / kTile;
-        release_fence();
+        if (a.nt_stores) release_fence();
         for (int pb = unpublished; pb <= lb; ++pb) {
           const BlockPos pp = pb == lb ? bp : block_of_position(a.order, w + pb * G, grid);
 #pragma unroll

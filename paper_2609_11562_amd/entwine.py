@@ -18,6 +18,8 @@ _lib = None
 OK, EINVAL, EUNSUPPORTED, ENOMEM, EHIP, ETIMEOUT = range(6)
 ORDER_INTERLEAVED, ORDER_ROW_MAJOR, ORDER_M_MAJOR = 0, 1, 2
 GEMM_256x256, GEMM_256x128, GEMM_128x256, GEMM_128x128 = 0, 1, 2, 3
+# release_blocks values other than a block count g >= 1
+RELEASE_AT_END, RELEASE_PARTITION, RELEASE_OUTPUT = -1, -2, -3
 GEMM_SHAPES = {GEMM_256x256: (256, 256), GEMM_256x128: (256, 128), GEMM_128x256: (128, 256),
                GEMM_128x128: (128, 128)}
 DEST_ALL = -1

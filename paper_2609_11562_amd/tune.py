@@ -71,7 +71,7 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
     """Time every valid configuration; returns (best, rows) where rows are
     dicts with the configuration, wall ms per call and median event time.
     With launch 0 (one kernel, reducers of 256 threads) b has no effect and
-    only its first value is tried."""
+    is recorded as 256."""
     import torch
 
     if scope == "layer" and launch != 0:
@@ -95,7 +95,8 @@ def sweep(workload: str, scope: str = "rank", xs=DEFAULT_XS, bs=DEFAULT_BS, cfgs
                      torch.empty(M // P, N, dtype=torch.bfloat16, device="cuda"))
         gs = torch.cuda.current_stream()
         rs = torch.cuda.Stream()
-        grid = list(itertools.product(cfgs, xs, bs[:1] if launch == 0 else bs, group_ms, release_blocks))
+        # the single launch's reducers are its own 256-thread workgroups
+        grid = list(itertools.product(cfgs, xs, (256,) if launch == 0 else bs, group_ms, release_blocks))
         for _ in range(passes):
             for gc, x, b, gm, g in grid:
                 kw = dict(gemm_cfg=gc, reduce_wgs=x, reduce_threads=b, group_m=gm, launch=launch, release_blocks=g,

@@ -78,7 +78,9 @@ def test_validate_config(lib):
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-1, launch=1)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(reduce_wgs=-2)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-1, store_mode=1)) == E.OK
-    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=E.RELEASE_PARTITION)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=E.RELEASE_OUTPUT)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-4)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(store_mode=2)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=1)) == E.OK
 

@@ -138,7 +138,11 @@ def test_results_independent_of_order_budget_threads_and_mode():
                    [dict(launch=1), dict(launch=1, reduce_threads=512, reduce_wgs=8),
                     dict(launch=1, gemm_cfg=3, reduce_threads=1024)] + \
                    [dict(launch=2), dict(launch=2, reduce_wgs=5), dict(launch=2, gemm_cfg=1, reduce_wgs=40)] + \
-                   [dict(reduce_wgs=-1), dict(reduce_wgs=-1, gemm_cfg=3)]
+                   [dict(reduce_wgs=-1), dict(reduce_wgs=-1, gemm_cfg=3)] + \
+                   [dict(release_blocks=g, launch=l, gemm_cfg=c)
+                    for g in (2, E.RELEASE_AT_END, E.RELEASE_PARTITION, E.RELEASE_OUTPUT)
+                    for l, c in ((0, 0), (1, 3), (2, 1))] + \
+                   [dict(release_blocks=E.RELEASE_PARTITION, reduce_wgs=-1, gemm_cfg=2)]
         for kw in variants:
             o = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(**kw)))
             assert np.array_equal(o, base), kw
@@ -151,6 +155,10 @@ def test_results_independent_of_order_budget_threads_and_mode():
         parts = [host_bits(run(ctx, A, B, peers, d, E.Config.make(reduce_wgs=x)))
                  for d, x in zip(range(P), (1, 3, 16, 64))]
         assert np.array_equal(np.concatenate(parts, axis=0), base), "chunks differ from all-chunk output"
+        # release groups on single chunks, each call leaving its counters at a multiple
+        for d, g in zip(range(P), (E.RELEASE_PARTITION, E.RELEASE_OUTPUT, E.RELEASE_PARTITION, 1)):
+            o = host_bits(run(ctx, A, B, peers, d, E.Config.make(release_blocks=g, gemm_cfg=d % 4)))
+            assert np.array_equal(o, base[d * (M // P):(d + 1) * (M // P)]), (d, g)
 
 
 def test_reducer_is_exact_on_given_partial():
@@ -208,8 +216,9 @@ def test_poisoned_buffers_never_leak_across_repeated_calls():
             A, B, peers = ups[i % 2]
             partial.fill_(nan)
             out.fill_(nan)
+            release = (1, 2, E.RELEASE_AT_END, E.RELEASE_PARTITION, E.RELEASE_OUTPUT)[i % 5]
             ctx.gemm_rs(A, B, peers, 5, out=out, partial=partial, reduce_stream=rs,
-                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 3))
+                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 3, release_blocks=release))
             got = host_bits(out)
             if i < 2:
                 check_rows(probs[i], got, out_global_rows(M, P, 5))

@@ -36,3 +36,14 @@ def test_write_entry_round_trip(tmp_path):
     assert t["llama7b_mlp_down_tp8"]["rank"]["reduce_wgs"] == 24
     assert t["llama7b_mlp_down_tp8"]["all"]["reduce_wgs"] == 32
     assert t["llama7b_mlp_down_tp8"]["rank"]["measured_ms"] == 0.5
+
+
+def test_ablation_studies_and_shapes():
+    from paper_2609_11562_amd import ablation
+    assert set(ablation.STUDIES) == {"order", "pool", "release", "budget"}
+    assert len(ablation.STUDIES["budget"][1]) == 8
+    for K in (512, 768, 4096):
+        w = ablation.workload(K)
+        assert (w.M, w.N, w.K, w.P) == (8192, 8192, K, 8)
+        cfg = E.Config.make(launch=1, gemm_cfg=E.GEMM_128x128, release_blocks=E.RELEASE_PARTITION, reduce_wgs=16)
+        assert E.validate(w.M, w.N, w.K, w.P, 0, cfg) == E.OK
