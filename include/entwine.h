@@ -188,6 +188,20 @@ entwine_status entwine_reduce_only(entwine_ctx* ctx, const void* partial, int64_
                                    const void* const* peers, int64_t ldp, int32_t dest, void* out,
                                    int64_t ldo, const entwine_config* cfg, void* stream);
 
+/* Per-workgroup timeline of the `back`-th most recent single-launch call
+ * made with record_timing (the computation window and communication tail of
+ * Section 5.3's figures, per CU): 4 device wall-clock stamps per workgroup
+ * {start, producer role end (= start if it had no producer work), first
+ * reduction task ready after its waits (0 if it reduced none, and always 0
+ * with the layer epilogue), end}, in workgroup order into `stamps`
+ * (host, `capacity` entries, at least 4 x nwgs).  nwgs: workgroups of the
+ * launch; nproducers: the first nproducers are producers; ticks_per_us: the
+ * stamps' clock.  With stamps == NULL only the counts are returned.
+ * ENTWINE_EUNSUPPORTED for a call without stamps (two-stream forms, or more
+ * than 1024 workgroups).  Blocks until the call completes. */
+entwine_status entwine_last_stamps(entwine_ctx* ctx, int32_t back, uint64_t* stamps, int32_t capacity,
+                                   int32_t* nwgs, int32_t* nproducers, double* ticks_per_us);
+
 /* Waits for the context's queued work, then reports the device status word:
  * returns ENTWINE_ETIMEOUT (with the tile and the flag source, -1 = local,
  * q = peer q) if any reducer wait expired since the previous query, else

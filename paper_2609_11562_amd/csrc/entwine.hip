@@ -61,7 +61,7 @@ struct entwine_ctx {
   uint64_t ticks_per_us = 100;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   TimingSlot ring[kRing];
-  unsigned long long* stamps = nullptr;   // kRing x kStampWgs x {start, producer end, end}, on first need
+  unsigned long long* stamps = nullptr;   // kRing x kStampWgs x kStampsPerWg, on first need
   unsigned int* task_ctr = nullptr;       // single launch: {next task, finished workgroups}, zero between calls
   unsigned long long* group_ctr = nullptr;  // release groups: tiles stored per partition (P) and output (1)
   int64_t ncalls = 0;          // calls with record_timing
@@ -296,6 +296,7 @@ GemmArgs gemm_args(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t l
   g.release_blocks = r.release_blocks;
   g.nt_stores = r.store_mode;
   g.group_ctr = ctx->group_ctr;
+  g.take_ctr = nullptr;
   return g;
 }
 
@@ -399,9 +400,8 @@ entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs&
                             const LayerArgs* layer = nullptr) {
   ReduceArgs ra = reduce_args(ctx, r, partial, ldc, peers, ldp, dest, out, ldo, epoch);
   ra.task_ctr = ctx->task_ctr;
-  // Dynamic tasks are half-tiles (reducer_dynamic).
-  ra.ntasks = 2 * tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
-  ra.ntasks_reduce = ra.ntasks;
+  ra.call_tiles = tiles_per_partition(int(ctx->M), int(ctx->N), ctx->P) * (dest == ENTWINE_DEST_ALL ? ctx->P : 1);
+  ra.ntasks = kTaskSplit * ra.call_tiles;   // reducer_dynamic
   if (layer) {
     // One task per output row (reducer_layer).
     ra.layer = 1;
@@ -417,14 +417,17 @@ entwine_status launch_fused(entwine_ctx* ctx, const Resolved& r, const GemmArgs&
   const int grid = G + r.x;
   unsigned long long* stamps = nullptr;
   if (ts && grid <= kStampWgs) {
-    if (!ctx->stamps) HIP_OR_FAIL(ctx, hipMalloc(&ctx->stamps, size_t(kRing) * kStampWgs * 3 * sizeof(unsigned long long)));
-    stamps = ctx->stamps + size_t(ts - ctx->ring) * kStampWgs * 3;
+    if (!ctx->stamps)
+      HIP_OR_FAIL(ctx, hipMalloc(&ctx->stamps, size_t(kRing) * kStampWgs * kStampsPerWg * sizeof(unsigned long long)));
+    stamps = ctx->stamps + size_t(ts - ctx->ring) * kStampWgs * kStampsPerWg;
     ts->has_stamps = true;
     ts->G = G;
     ts->grid = grid;
   }
   FusedKernel k = ctx->K % GemmShape<128, 128>::BK ? fused_kernel_t<true>(r.gemm_cfg) : fused_kernel_t<false>(r.gemm_cfg);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, g, ra, G, ctx->P, stamps);
+  GemmArgs gf = g;
+  gf.take_ctr = ctx->task_ctr;   // producers take their first reduction task early
+  hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, gf, ra, G, ctx->P, stamps);
   HIP_OR_FAIL(ctx, hipGetLastError());
   return ENTWINE_OK;
 }
@@ -746,14 +749,14 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
     // from the first workgroup's start; end to end from the events around it.
     HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
     HIP_OR_FAIL(ctx, hipEventElapsedTime(&e, s.start, s.red_end));
-    std::vector<unsigned long long> h(size_t(s.grid) * 3);
-    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * 3,
+    std::vector<unsigned long long> h(size_t(s.grid) * kStampsPerWg);
+    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * kStampsPerWg,
                                h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
     unsigned long long t0 = ~0ull, ge = 0, re = 0;
     for (int b = 0; b < s.grid; ++b) {
-      t0 = std::min(t0, h[3 * b]);
-      if (b < s.G) ge = std::max(ge, h[3 * b + 1]);
-      re = std::max(re, h[3 * b + 2]);
+      t0 = std::min(t0, h[kStampsPerWg * b]);
+      if (b < s.G) ge = std::max(ge, h[kStampsPerWg * b + 1]);
+      re = std::max(re, h[kStampsPerWg * b + 3]);
     }
     const double per_ms = double(ctx->ticks_per_us) * 1e3;
     g = float(double(ge - t0) / per_ms);
@@ -775,6 +778,23 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
   if (gemm_ms) *gemm_ms = g;
   if (reduce_ms) *reduce_ms = rd;
   if (e2e_ms) *e2e_ms = e;
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_last_stamps(entwine_ctx* ctx, int32_t back, uint64_t* stamps, int32_t capacity,
+                                   int32_t* nwgs, int32_t* nproducers, double* ticks_per_us) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  if (back < 0 || back >= kRing || back >= ctx->ncalls) return fail(ctx, ENTWINE_EINVAL, "no such timed call");
+  const TimingSlot& s = ctx->ring[(ctx->ncalls - 1 - back) % kRing];
+  if (!s.has_stamps) return fail(ctx, ENTWINE_EUNSUPPORTED, "the call has no workgroup timestamps");
+  if (nwgs) *nwgs = s.grid;
+  if (nproducers) *nproducers = s.G;
+  if (ticks_per_us) *ticks_per_us = double(ctx->ticks_per_us);
+  if (!stamps) return ENTWINE_OK;
+  if (capacity < s.grid * kStampsPerWg) return fail(ctx, ENTWINE_EINVAL, "capacity below %d", s.grid * kStampsPerWg);
+  HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
+  HIP_OR_FAIL(ctx, hipMemcpy(stamps, ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * kStampsPerWg,
+                             size_t(s.grid) * kStampsPerWg * sizeof(uint64_t), hipMemcpyDeviceToHost));
   return ENTWINE_OK;
 }
 

@@ -81,6 +81,7 @@ struct GemmArgs {
   int nt_stores;          // 1: non-temporal tile stores (written back at the release); 0: write-through
   unsigned long long* group_ctr;   // release groups: tiles stored, per partition (P) then the output (1);
                                    // a multiple of the group's tile count between calls
+  unsigned int* take_ctr;  // fused launch: the reduction task counter, first taken during the last epilogue
 };
 
 constexpr int kReleasePartition = -2;
@@ -218,7 +219,10 @@ __device__ __forceinline__ void store16_wt(void* dst, u32x4_t v) {
 // LDS, 1 KB aligned.  Used by gemm_producer and by the single-launch fused
 // kernel, whose first G workgroups are producers.
 template <int BM, int BN, bool TAIL>
-__device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, const int G, char* smem) {
+// Returns, in thread 0 when a.take_ctr is set and the workgroup had blocks,
+// the reduction task it took at the start of its last epilogue (the atomic's
+// round trip then overlaps the epilogue); ~0u otherwise.
+__device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const int w, const int G, char* smem) {
   using S = GemmShape<BM, BN>;
   constexpr int NS = S::STAGES;
   constexpr int D = S::DMA, DH = S::DH;
@@ -239,7 +243,7 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
   const int K = a.K;
   const int nk = (K + S::BK - 1) / S::BK;
   const int total = mine * nk;
-  if (total == 0) return;
+  if (total == 0) return ~0u;
 
   // ---- per-lane load sources: byte offsets inside a block, and their K.
   // A: one load fills 16 rows of 64 bytes; lane -> row lane / 4, stored
@@ -458,6 +462,7 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
   char* const cst = smem + NS * S::STAGE + wave * (32 * ROWB);
 
   int g = 0;
+  unsigned int taken = ~0u;
   int unpublished = 0;   // first of this workgroup's blocks whose tiles are not yet published
   for (int lb = 0; lb < mine; ++lb) {
     const BlockPos bp = block_of_position(a.order, w + lb * G, grid);
@@ -468,6 +473,8 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
     for (int kt = 0; kt < nk; ++kt) step(g++);
+
+    if (a.take_ctr && tid == 0 && lb + 1 == mine) taken = atomicAdd(a.take_ctr, 1u);
 
     // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
     // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T): 4
@@ -561,6 +568,7 @@ __device__ __forceinline__ void producer_body(const GemmArgs& a, const int w, co
   }
   // Loads past the end of the stream may still be writing LDS.
   if (!TAIL) wait_vm<0>();
+  return taken;
 }
 
 template <int BM, int BN, bool TAIL>

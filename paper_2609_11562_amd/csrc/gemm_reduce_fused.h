@@ -21,8 +21,11 @@
 
 namespace entwine {
 
-// stamps: null, or 3 per workgroup {start, producer end, end} in wall-clock
-// ticks (producer end = start for workgroups without producer work).
+constexpr int kStampsPerWg = 4;
+
+// stamps: null, or kStampsPerWg per workgroup in wall-clock ticks: {start,
+// producer end (= start without producer work), first reduction task ready
+// (0 if none), end}.
 template <int BM, int BN, bool TAIL>
 __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs r, int G, int np,
                                                           unsigned long long* stamps) {
@@ -30,39 +33,41 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   const unsigned long long t0 = stamps ? wall_clock64() : 0;
   const int b = blockIdx.x;
   publish_peer_slice(r, np, b, gridDim.x);
-  if (b < G) producer_body<BM, BN, TAIL>(g, b, G, smem);
+  const unsigned int taken = b < G ? producer_body<BM, BN, TAIL>(g, b, G, smem) : ~0u;
   const unsigned long long t1 = stamps ? wall_clock64() : 0;
   int* s = reinterpret_cast<int*>(smem);
   static_assert(kLayerThreads == 256, "the layer tasks run on the fused launch's workgroups");
   if (r.layer) {
     switch (np) {
-      case 1: reducer_layer<1>(r, s); break;
-      case 2: reducer_layer<2>(r, s); break;
-      case 3: reducer_layer<3>(r, s); break;
-      case 4: reducer_layer<4>(r, s); break;
-      case 5: reducer_layer<5>(r, s); break;
-      case 6: reducer_layer<6>(r, s); break;
-      case 7: reducer_layer<7>(r, s); break;
-      default: reducer_layer<8>(r, s); break;
+      case 1: reducer_layer<1>(r, s, taken); break;
+      case 2: reducer_layer<2>(r, s, taken); break;
+      case 3: reducer_layer<3>(r, s, taken); break;
+      case 4: reducer_layer<4>(r, s, taken); break;
+      case 5: reducer_layer<5>(r, s, taken); break;
+      case 6: reducer_layer<6>(r, s, taken); break;
+      case 7: reducer_layer<7>(r, s, taken); break;
+      default: reducer_layer<8>(r, s, taken); break;
     }
   } else {
+    unsigned long long* ready = stamps ? stamps + kStampsPerWg * b + 2 : nullptr;
     switch (np) {
-      case 1: reducer_dynamic<256, 1>(r, s); break;
-      case 2: reducer_dynamic<256, 2>(r, s); break;
-      case 3: reducer_dynamic<256, 3>(r, s); break;
-      case 4: reducer_dynamic<256, 4>(r, s); break;
-      case 5: reducer_dynamic<256, 5>(r, s); break;
-      case 6: reducer_dynamic<256, 6>(r, s); break;
-      case 7: reducer_dynamic<256, 7>(r, s); break;
-      default: reducer_dynamic<256, 8>(r, s); break;
+      case 1: reducer_dynamic<256, 1, kTaskSplit>(r, s, ready, taken); break;
+      case 2: reducer_dynamic<256, 2, kTaskSplit>(r, s, ready, taken); break;
+      case 3: reducer_dynamic<256, 3, kTaskSplit>(r, s, ready, taken); break;
+      case 4: reducer_dynamic<256, 4, kTaskSplit>(r, s, ready, taken); break;
+      case 5: reducer_dynamic<256, 5, kTaskSplit>(r, s, ready, taken); break;
+      case 6: reducer_dynamic<256, 6, kTaskSplit>(r, s, ready, taken); break;
+      case 7: reducer_dynamic<256, 7, kTaskSplit>(r, s, ready, taken); break;
+      default: reducer_dynamic<256, 8, kTaskSplit>(r, s, ready, taken); break;
     }
   }
   if (stamps) {
     __syncthreads();
     if (threadIdx.x == 0) {
-      stamps[3 * b] = t0;
-      stamps[3 * b + 1] = b < G ? t1 : t0;
-      stamps[3 * b + 2] = wall_clock64();
+      stamps[kStampsPerWg * b] = t0;
+      stamps[kStampsPerWg * b + 1] = b < G ? t1 : t0;
+      if (r.layer) stamps[kStampsPerWg * b + 2] = 0;
+      stamps[kStampsPerWg * b + 3] = wall_clock64();
     }
   }
 }

@@ -46,7 +46,7 @@ struct ReduceArgs {
   int withhold_peer;       // with publish_peers: peer left unpublished, or -1
   unsigned int* task_ctr;  // dynamic tasks: {next task, finished workgroups}
   int ntasks;              // dynamic tasks of this call
-  int ntasks_reduce;       // half-tiles the call reduces (their peer flags are published)
+  int call_tiles;          // tiles the call reduces (their peer flags are published)
   // Layer epilogue (residual addition + RMSNorm after the reduce-scatter):
   // tasks are output rows; `out` receives the residual stream h = sum +
   // residual and `y` the normalised rows.
@@ -81,6 +81,11 @@ constexpr int pow2_floor(int v) {
   while (p * 2 <= v) p *= 2;
   return p;
 }
+
+// Dynamic reduction tasks are 1 / kTaskSplit of a tile (kTile / kTaskSplit
+// rows): small enough that the end of a call, when every workgroup reduces,
+// splits evenly, large enough to keep each lane's loads in flight.
+constexpr int kTaskSplit = 2;
 
 // Flag polled by lane `lane` of a waiting wave for global tile gt: lane 0
 // the local flag, lane q+1 peer q's.
@@ -225,13 +230,13 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
 }
 
 // Publishes, as part of one launch, the synthetic peers' flags of every tile
-// the call reduces (a.ntasks_reduce / 2 tiles: the reduce tasks are half-tiles),
+// the call reduces (a.call_tiles),
 // split over all nb workgroups; peer `withhold_peer` stays unpublished.
 __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, int b, int nb) {
   const BlockGrid grid = make_grid(a.M, a.N, np, a.BM, a.BN, a.group_m);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
-  const int call_tiles = a.ntasks_reduce / 2;
+  const int call_tiles = a.call_tiles;
   const int64_t n = static_cast<int64_t>(np - 1) * call_tiles;
   for (int64_t i = static_cast<int64_t>(b) * blockDim.x + threadIdx.x; i < n;
        i += static_cast<int64_t>(nb) * blockDim.x) {
@@ -256,14 +261,16 @@ __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, 
 // finish returns both counters to zero, ready for the next call.  After a
 // timeout waits are skipped (the call's output is then undefined) but the
 // task accounting stays exact.  s: two ints of LDS.
-template <int THREADS, int NP>
-__device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
+template <int THREADS, int NP, int SPLIT>
+__device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s, unsigned long long* first_ready,
+                                                unsigned int taken) {
+  static_assert(kTile % SPLIT == 0 && SPLIT >= 1, "a task is kTile / SPLIT rows of a tile");
   const BlockGrid grid = make_grid(a.M, a.N, NP, a.BM, a.BN, a.group_m);
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
   const int lane = threadIdx.x & 63;
   auto task_tile = [&](int task) {
-    const int u = task >> 1;
+    const int u = task / SPLIT;
     const int part = a.dest >= 0 ? a.dest : u % NP;
     const int idx = a.dest >= 0 ? u : u / NP;
     int tr, tc;
@@ -271,24 +278,34 @@ __device__ __forceinline__ void reducer_dynamic(const ReduceArgs& a, int* s) {
     return tr * tiles_n + tc;
   };
   __syncthreads();   // producer waves are done with the LDS
-  if (threadIdx.x == 0) s[0] = static_cast<int>(atomicAdd(a.task_ctr, 1u));
+  if (threadIdx.x == 0) s[0] = static_cast<int>(taken != ~0u ? taken : atomicAdd(a.task_ctr, 1u));
   __syncthreads();
   int task = s[0];
   bool timed_out = false;   // wave 0
+  if (first_ready && threadIdx.x == 0) *first_ready = 0;
   while (task < a.ntasks) {
     const int gt = task_tile(task);
-    const int row0 = (task & 1) * (kTile / 2);
+    const int row0 = (task % SPLIT) * (kTile / SPLIT);
     if (threadIdx.x < 64) {
-      if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
+      // The next task is taken now and stored once this one's flags are in,
+      // so the two round trips overlap.
+      const unsigned int nxt = threadIdx.x == 0 ? atomicAdd(a.task_ctr, 1u) : 0u;
       if (!timed_out) {
         const int seen = lane < NP ? poll_relaxed(flag_of_lane(a, lane, ntiles, gt)) : static_cast<int>(a.epoch);
         timed_out = !wave_await_tile(a, gt, ntiles, NP, seen, 8);
       }
-      if (lane == 0) acquire_fence();
+      if (lane == 0) {
+        acquire_fence();
+        s[1] = static_cast<int>(nxt);
+      }
     }
     __syncthreads();
+    if (first_ready && threadIdx.x == 0) {
+      *first_ready = wall_clock64();
+      first_ready = nullptr;
+    }
     const int next = s[1];
-    reduce_tile<THREADS, NP, kTile / 2>(a, gt, tiles_n, row0, [] {});
+    reduce_tile<THREADS, NP, kTile / SPLIT>(a, gt, tiles_n, row0, [] {});
     __syncthreads();   // s[1] is rewritten next
     task = next;
   }
@@ -460,14 +477,14 @@ __device__ __forceinline__ void layer_row(const ReduceArgs& a, int64_t orow, flo
 // row are published; counters returned to zero as in reducer_dynamic.
 // s: eight ints of LDS.
 template <int NP>
-__device__ __forceinline__ void reducer_layer(const ReduceArgs& a, int* s) {
+__device__ __forceinline__ void reducer_layer(const ReduceArgs& a, int* s, unsigned int taken) {
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
   const int64_t first_row = a.dest >= 0 ? static_cast<int64_t>(a.dest) * (a.M / NP) : 0;
   auto tile_row = [&](int task) { return static_cast<int>((first_row + task) / kTile); };
   float* red = reinterpret_cast<float*>(s + 4);
   __syncthreads();   // producer waves are done with the LDS
-  if (threadIdx.x == 0) s[0] = static_cast<int>(atomicAdd(a.task_ctr, 1u));
+  if (threadIdx.x == 0) s[0] = static_cast<int>(taken != ~0u ? taken : atomicAdd(a.task_ctr, 1u));
   __syncthreads();
   int task = s[0];
   bool timed_out = false;              // wave 0

@@ -70,6 +70,8 @@ _PROTOS = {
     "entwine_query_status": (_i32, [_vp, _P32, _P32, _P32]),
     "entwine_last_timing": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
+    "entwine_last_stamps": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_uint64), _i32, _P32, _P32,
+                                   ctypes.POINTER(ctypes.c_double)]),
     "entwine_validate": (_i32, [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(Config)]),
     "entwine_tile_schedule": (_i32, [_i32, _i64, _i64, _i32, _i32, _i32, _i32, _P32, _P32]),
     "entwine_consumer_tasks": (_i32, [_i32, _i32, _i32, _i32, _i32, _P32, _P32, _i32, _P32]),
@@ -272,6 +274,23 @@ class Context:
         if s not in (OK, ETIMEOUT):
             _check(s, self._h)
         return s, tile.value, src.value
+
+    def last_stamps(self, back: int = 0):
+        """Per-workgroup timeline of a single-launch call made with
+        record_timing=1: (stamps, nproducers) with stamps an (nwgs, 4) float
+        array of microseconds since the first workgroup's start, columns
+        start, producer end, first reduction task ready (NaN if none), end."""
+        import numpy as np
+        n, g, tpu = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_double()
+        _check(lib().entwine_last_stamps(self._h, back, None, 0, ctypes.byref(n), ctypes.byref(g), ctypes.byref(tpu)),
+               self._h)
+        buf = (ctypes.c_uint64 * (4 * n.value))()
+        _check(lib().entwine_last_stamps(self._h, back, buf, len(buf), None, None, None), self._h)
+        raw = np.frombuffer(buf, dtype=np.uint64).reshape(n.value, 4)
+        t0 = raw[:, 0].min()
+        us = (raw.astype(np.float64) - float(t0)) / tpu.value
+        us[raw[:, 2] == 0, 2] = np.nan
+        return us, g.value
 
     def last_timing(self, back: int = 0):
         """(gemm_ms, reduce_ms, e2e_ms) of a call made with record_timing=1."""

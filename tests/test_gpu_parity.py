@@ -267,3 +267,19 @@ def test_full_size_workloads_on_sampled_rows(name):
                 check_rows(prob, host_bits(o[torch.as_tensor(local, device="cuda")]), grow)
     del A, B, peers
     torch.cuda.empty_cache()
+
+
+def test_workgroup_timeline_is_consistent(tiny):
+    w, prob, ctx, (A, B, peers) = tiny
+    print("[stamps]", flush=True)
+    run(ctx, A, B, peers, 1, E.Config.make(record_timing=1, reduce_wgs=4))
+    us, G = ctx.last_stamps()
+    assert us.shape[1] == 4 and 0 < G < us.shape[0]
+    assert np.all(us[:, 0] >= 0) and np.all(us[:, 1] >= us[:, 0]) and np.all(us[:, 3] >= us[:, 1])
+    ready = ~np.isnan(us[:, 2])
+    assert ready.any() and np.all(us[ready, 2] >= us[ready, 1]) and np.all(us[ready, 2] <= us[ready, 3])
+    assert np.all(us[G:, 1] == us[G:, 0])   # dedicated reducers have no producer role
+    run(ctx, A, B, peers, 1, E.Config.make(record_timing=1, launch=1))
+    with pytest.raises(E.EntwineError) as ei:
+        ctx.last_stamps()
+    assert ei.value.status == E.EUNSUPPORTED
