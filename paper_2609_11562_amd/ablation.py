@@ -21,8 +21,12 @@ ablations (Section 5.3):
               {2048, 4096, 8192}.
 * ``budget``  the communication-budget sweep (Appendix B): GEMM window, tail
               and end-to-end latency against x for eight values of K.
+* ``range``   the operating range (Section 5.4.1): both workload suites of
+              Table 1, each with its GEMM wave count (256 x 256 producer
+              blocks per CU), the single launch at its best budget and the
+              non-overlapped baseline.
 
-M = N = 8192 and P = 8 throughout.  Every row reports the wall-clock latency
+M = N = 8192 and P = 8 throughout, except in ``range``.  Every row reports the wall-clock latency
 per call (median over rounds of ``steps`` calls), the producer's window and
 the tail from the call's own event / device timestamps, and the speedup over
 the non-overlapped baseline (GEMM, then reduction with the whole device, on
@@ -40,7 +44,7 @@ import time
 
 from . import entwine as E
 from .inputs import bits_to_torch
-from .workloads import WORKLOADS, _llm
+from .workloads import SUITES, WORKLOADS, _llm
 
 M_ABL, N_ABL, P_ABL = 8192, 8192, 8
 BUDGETS = (4, 8, 16, 24, 32, 48, 64)
@@ -182,7 +186,23 @@ def study_budget(ks, budgets, emit, **tk):
         b.close()
 
 
-STUDIES = {"order": (study_order, (512, 2048)), "pool": (study_pool, (512, 2048)),
+def study_range(ks, budgets, emit, **tk):
+    """ks: unused (the suites fix K)."""
+    del ks
+    for suite in ("models", "main"):
+        for name in SUITES[suite]:
+            w = WORKLOADS[name]
+            b = Bench(w, **tk)
+            base = baseline(b)
+            best, _ = best_over_budgets(b, (-1,) + tuple(x for x in budgets if x in (16, 32)), release_blocks=2)
+            waves = (w.M // 256) * (w.N // 256) / 256.0
+            emit({"study": "range", "suite": suite, "workload": name, "M": w.M, "N": w.N, "K": w.K, "waves": waves,
+                  **best, "baseline_gemm_ms": base["gemm_window_ms"], "baseline_ms": base["ms"],
+                  "speedup": round(base["ms"] / best["ms"], 3)})
+            b.close()
+
+
+STUDIES = {"order": (study_order, (512, 2048)), "pool": (study_pool, (512, 2048)), "range": (study_range, ()),
            "release": (study_release, (2048, 4096, 8192)),
            "budget": (study_budget, (256, 512, 768, 1024, 1536, 2048, 3072, 4096))}
 

@@ -75,7 +75,30 @@ for _S in (4, 8, 16):
               f"attention output + residual addition + RMSNorm, {_S}K tokens", layer=True)
     WORKLOADS[_w.name] = _w
 
+# The paper's two evaluation suites (Table 1), one rank's share at P = 8.
+# Main operator suite: N = 8192 (Llama-3-70B width) with M in {8192, 16384,
+# 32768, 49152} and N = 16384 (Llama-3.1-405B width) with M = 16384, each at
+# K_local in {2048, 4096, 8192}: 15 workloads.
+SUITES = {"main": [], "models": []}
+for _N, _Ms in ((8192, (8192, 16384, 32768, 49152)), (16384, (16384,))):
+    for _M in _Ms:
+        for _K in (2048, 4096, 8192):
+            _w = _llm(f"main_{_M}x{_K}x{_N}_p8", _M, _K, _N, 8, "main operator suite")
+            WORKLOADS[_w.name] = _w
+            SUITES["main"].append(_w.name)
+# Model-derived suite at TP = 8: five projections (N, K_local) at logical M in
+# {512, ..., 8192}; M = 512 runs padded to 1024 rows, as the paper's methods
+# do: 25 workloads.
+for _p, _N, _K in (("llama3_8b_attn_out", 4096, 512), ("llama3_8b_mlp_down", 4096, 1792),
+                   ("llama3_70b_attn_out", 8192, 1024), ("llama3_70b_mlp_down", 8192, 3584),
+                   ("qwen25_72b_mlp_down", 8192, 3696)):
+    for _M in (512, 1024, 2048, 4096, 8192):
+        _w = _llm(f"{_p}_m{_M}_tp8", max(_M, 1024), _K, _N, 8,
+                  f"model-derived suite, logical M = {_M}" + (" (padded to 1024 rows)" if _M < 1024 else ""))
+        WORKLOADS[_w.name] = _w
+        SUITES["models"].append(_w.name)
+
 BENCH_WORKLOAD = "llama7b_mlp_down_tp8"
 SMALL_WORKLOAD = "tiny_512x256x1024_p2"
 
-__all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "SMALL_WORKLOAD", "BASE_SEED"]
+__all__ = ["Workload", "WORKLOADS", "SUITES", "BENCH_WORKLOAD", "SMALL_WORKLOAD", "BASE_SEED"]

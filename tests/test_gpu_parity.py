@@ -249,7 +249,8 @@ def sample_rows(M, P, dest, n=24, seed=0):
 
 
 @pytest.mark.parametrize("name", ["llama7b_mlp_down_tp8", "llama70b_attn_out_tp8", "llama70b_mlp_down_tp8",
-                                  "sweep_8192x512x8192_p2", "sweep_8192x2048x8192_p4"])
+                                  "sweep_8192x512x8192_p2", "sweep_8192x2048x8192_p4",
+                                  "qwen25_72b_mlp_down_m512_tp8", "llama3_8b_attn_out_m2048_tp8"])
 def test_full_size_workloads_on_sampled_rows(name):
     w = WORKLOADS[name]
     print(f"[full] {name}", flush=True)

@@ -40,10 +40,22 @@ def test_write_entry_round_trip(tmp_path):
 
 def test_ablation_studies_and_shapes():
     from paper_2609_11562_amd import ablation
-    assert set(ablation.STUDIES) == {"order", "pool", "release", "budget"}
+    assert set(ablation.STUDIES) == {"order", "pool", "release", "budget", "range"}
     assert len(ablation.STUDIES["budget"][1]) == 8
     for K in (512, 768, 4096):
         w = ablation.workload(K)
         assert (w.M, w.N, w.K, w.P) == (8192, 8192, K, 8)
         cfg = E.Config.make(launch=1, gemm_cfg=E.GEMM_128x128, release_blocks=E.RELEASE_PARTITION, reduce_wgs=16)
         assert E.validate(w.M, w.N, w.K, w.P, 0, cfg) == E.OK
+
+
+def test_paper_suites_have_table_1_shapes():
+    from paper_2609_11562_amd.workloads import SUITES
+    main = [WORKLOADS[n] for n in SUITES["main"]]
+    assert len(main) == 15 and {w.K for w in main} == {2048, 4096, 8192}
+    assert {(w.M, w.N) for w in main} == {(8192, 8192), (16384, 8192), (32768, 8192), (49152, 8192), (16384, 16384)}
+    models = [WORKLOADS[n] for n in SUITES["models"]]
+    assert len(models) == 25 and min(w.M for w in models) == 1024
+    assert {(w.N, w.K) for w in models} == {(4096, 512), (4096, 1792), (8192, 1024), (8192, 3584), (8192, 3696)}
+    for w in main + models:
+        assert E.validate(w.M, w.N, w.K, w.P, 0, E.Config.make()) == E.OK, w.name
