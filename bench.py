@@ -135,6 +135,9 @@ def main():
         if v is not None:
             kw[k] = v
     cfg = E.Config.make(**kw, record_timing=1)
+    # The non-overlapped legs give the reduction the whole device (two-stream
+    # kernels, budget capped by the library at min(tiles per chunk, CUs - 1)).
+    cfg_seq = E.Config.make(**dict(kw, launch=1, reduce_wgs=255, reduce_threads=1024), record_timing=1)
 
     def dest_of(i):
         if all_chunks:
@@ -168,16 +171,16 @@ def main():
         elif mode in ("fused", "plain"):
             ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
         elif mode == "seq":
-            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=gs)
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg_seq, gemm_stream=gs, reduce_stream=gs)
         elif mode == "layer_unfused":
             # sequential GEMM + reduction, then the epilogue as separate device operations
-            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=gs)
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg_seq, gemm_stream=gs, reduce_stream=gs)
             h = torch.add(outs[d], lay["R"], out=lay["h_unfused"][d])
             lay["y_unfused"][d] = torch.nn.functional.rms_norm(h, (N,), lay["gamma"], lay["eps"])
         elif mode == "gemm":
             ctx.gemm_only(A, B, partial=partial, cfg=cfg, stream=gs)
         else:
-            ctx.reduce_only(partial, peers, d, out=outs[d], cfg=cfg, stream=gs)
+            ctx.reduce_only(partial, peers, d, out=outs[d], cfg=cfg_seq, stream=gs)
 
     def timed(mode, steps, warmup):
         for i in range(warmup):
