@@ -60,32 +60,26 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_sources_hash(root: str) -> str:
-    """First 16 hex digits of the SHA-256 over the HIP sources and the ABI
-    header, in a fixed order; identifies the kernels a counter run measured."""
-    import glob
+def library_hash(root: str) -> str:
+    """First 16 hex digits of the SHA-256 of the built library: identifies
+    the kernels a counter run measured (the build is deterministic, so edits
+    that do not change the machine code keep the hash)."""
     import hashlib
-    pkg = os.path.join(root, "paper_2609_11562_amd", "csrc")
-    files = sorted(glob.glob(os.path.join(pkg, "*.h"))) + sorted(glob.glob(os.path.join(pkg, "*.hip"))) + \
-        [os.path.join(root, "include", "entwine.h")]
-    h = hashlib.sha256()
-    for f in files:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
+    with open(os.path.join(root, "paper_2609_11562_amd", "libentwine.so"), "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
 def measured_traffic(root: str, workload: str, kernel: str, cfg_now: dict):
     """HBM bytes per launch of the dominant kernel from the recorded counter
     runs (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by the same
     counter's reading on a device copy of known size), or None when none was
-    taken for this workload, kernel, configuration and kernel sources."""
+    taken for this workload, kernel, configuration and built library."""
     path = os.path.join(root, "paper_2609_11562_amd", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         e = json.load(f).get(workload)
-    if not e or not e["kernel"].startswith(kernel) or e["sources_sha256_16"] != kernel_sources_hash(root):
+    if not e or not e["kernel"].startswith(kernel) or e["library_sha256_16"] != library_hash(root):
         return None
     if any(cfg_now.get(k) != v for k, v in e["config"].items()):
         return None

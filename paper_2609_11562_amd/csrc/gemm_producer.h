@@ -217,11 +217,11 @@ __device__ __forceinline__ void store16_wt(void* dst, u32x4_t v) {
 // real slab uses again; they are drained before the kernel ends.
 // The producer role of workgroup w of G; `smem` is GemmShape::LDS_BYTES of
 // LDS, 1 KB aligned.  Used by gemm_producer and by the single-launch fused
-// kernel, whose first G workgroups are producers.
+// kernel, whose first G workgroups are producers.  Returns, in thread 0 when
+// a.take_ctr is set and the workgroup had blocks, the reduction task it took
+// at the start of its last epilogue (the atomic's round trip then overlaps
+// the epilogue); ~0u otherwise.
 template <int BM, int BN, bool TAIL>
-// Returns, in thread 0 when a.take_ctr is set and the workgroup had blocks,
-// the reduction task it took at the start of its last epilogue (the atomic's
-// round trip then overlaps the epilogue); ~0u otherwise.
 __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const int w, const int G, char* smem) {
   using S = GemmShape<BM, BN>;
   constexpr int NS = S::STAGES;
