@@ -322,8 +322,8 @@ def main():
 def cpu_baseline(prob, w, outs, all_chunks, dest_of, lay=None):
     """The CPU oracle, as it stands, timed on the host: every chunk of the
     workload (the whole job; with the layer epilogue, each chunk followed by
-    the residual addition and RMSNorm), repeated until about 10 s have elapsed
-    or three runs are done.  Also compares the GPU's last outputs (y for the
+    the residual addition and RMSNorm), repeated for about 10 s (at least
+    three runs).  Also compares the GPU's last outputs (y for the
     layer workloads) on sampled rows of chunk 0."""
     import numpy as np
     import oracle
@@ -336,7 +336,7 @@ def cpu_baseline(prob, w, outs, all_chunks, dest_of, lay=None):
         threads = None
     runs = []
     t_end = time.perf_counter() + 10.0
-    while len(runs) < 3 and (not runs or time.perf_counter() < t_end):
+    while len(runs) < 3 or (time.perf_counter() < t_end and len(runs) < 500):
         t0 = time.perf_counter()
         C = oracle.local_partial(prob.A, prob.B)
         for d in range(w.P):
@@ -362,7 +362,8 @@ def cpu_baseline(prob, w, outs, all_chunks, dest_of, lay=None):
     what = "reduce-scatter" + (" + residual addition + RMSNorm" if lay is not None else "")
     return {"value": round(w.flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "seconds_per_job": round(t, 3), "runs": len(runs),
-            "sample": f"whole job ({w.name}, all {w.P} chunks, {what}, fp64 numpy), median of {len(runs)} runs",
+            "sample": f"whole job ({w.name}, all {w.P} chunks, {what}, fp64 numpy), median of {len(runs)} runs "
+                      f"({sum(runs):.1f} s of CPU work)",
             "gpu_spot_check": {"rows": int(len(rows)), "output": "y" if lay is not None else "out",
                                "max_abs_err": float(np.abs(got - ref).max()),
                                "within_bound": bool(np.all(np.abs(got - ref) <= bound)),

@@ -126,3 +126,20 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(E, "_lib", None)
     with pytest.raises(ImportError):
         E.lib()
+
+
+def test_header_is_plain_c(tmp_path):
+    """The ABI header compiles as C (no C++ types leak into the boundary)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    src.write_text('#include "entwine.h"\n'
+                   'int main(void) { entwine_config c; entwine_config_default(&c);\n'
+                   '  return entwine_abi_version() == ENTWINE_ABI_VERSION && c.launch == 0 ? 0 : 1; }\n')
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-I", inc, str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
