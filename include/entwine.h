@@ -109,16 +109,17 @@ typedef struct {
                              1 and 0 partition the CUs instead */
   int32_t release_blocks; /* g: a producer workgroup publishes its finished
                              tiles after every g of its blocks, one release
-                             fence each time (Section 5.3.2, release
-                             granularity); 0 = default = 1; -1 = only once,
+                             each time (Section 5.3.2, release granularity:
+                             every wave waits for its tile stores, plus an
+                             L2 write-back with store_mode 1); 0 = default = 1; -1 = only once,
                              after its last block; release groups, where a
                              tile's flag waits for its whole group:
                              -2 = its row partition (chunk), -3 = the whole
                              output (the coarse end of Section 5.3.2's
                              ablation) */
-  int32_t store_mode;     /* partial tile stores: 0 = write-through (the
-                             release has little dirty data to write back),
-                             1 = non-temporal (written back by the release) */
+  int32_t store_mode;     /* partial tile stores: 0 = write-through (a
+                             release only waits for them), 1 = non-temporal
+                             (written back from L2 by the release) */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */
@@ -132,13 +133,15 @@ entwine_status entwine_ctx_create(entwine_ctx** out, int32_t device, int64_t M, 
                                   int64_t K, int32_t P);
 entwine_status entwine_ctx_destroy(entwine_ctx* ctx);
 
-/* The fused path (Sections 3.1-3.2, 4.1-4.3).  Enqueues, after the prior
- * work on gemm_stream: the producer GEMM (tiles in cfg->order, a release
- * flag per 128 x 128 tile) on gemm_stream, and the synthetic peer-flag
- * publication plus the tile reducer (grid x, b threads) on reduce_stream;
- * the two kernels run concurrently.  On return gemm_stream is ordered after
- * both.  When reduce_stream == gemm_stream the two run one after the other
- * (the unfused baseline).
+/* The fused path (Sections 3.1-3.2, 4.1-4.3), enqueued after the prior work
+ * on gemm_stream: the producer GEMM (tiles in cfg->order, a ready flag per
+ * 128 x 128 tile), the synthetic peers' flag publication and the tile
+ * reduction, concurrently.  With cfg->launch 0 (default) both roles are one
+ * kernel launch on gemm_stream; with 1 and 2 the producer runs on
+ * gemm_stream and the reducer on reduce_stream.  On return gemm_stream is
+ * ordered after all of it.  When reduce_stream == gemm_stream the GEMM and
+ * the reduction (two-stream kernels) run one after the other instead (the
+ * unfused baseline).
  *   dest in [0, P): out is (M/P) x N, chunk dest (one rank's share);
  *   dest == ENTWINE_DEST_ALL: out is M x N, every chunk.
  *   peers: host array of P-1 device pointers, each an M x N matrix with
