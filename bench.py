@@ -132,6 +132,8 @@ def main():
     # The non-overlapped legs give the reduction the whole device (two-stream
     # kernels, budget capped by the library at min(tiles per chunk, CUs - 1)).
     cfg_seq = E.Config.make(**dict(kw, launch=1, reduce_wgs=255, reduce_threads=1024), record_timing=1)
+    # the producer alone in the partition-contiguous order (the plain GEMM's)
+    cfg_rm = E.Config.make(**dict(kw, order=E.ORDER_ROW_MAJOR), record_timing=1)
 
     def dest_of(i):
         if all_chunks:
@@ -173,6 +175,8 @@ def main():
             lay["y_unfused"][d] = torch.nn.functional.rms_norm(h, (N,), lay["gamma"], lay["eps"])
         elif mode == "gemm":
             ctx.gemm_only(A, B, partial=partial, cfg=cfg, stream=gs)
+        elif mode == "gemm_row_major":
+            ctx.gemm_only(A, B, partial=partial, cfg=cfg_rm, stream=gs)
         else:
             ctx.reduce_only(partial, peers, d, out=outs[d], cfg=cfg_seq, stream=gs)
 
@@ -224,6 +228,7 @@ def main():
         _, p_r = timed("reduce", n_leg, w_leg)
         seq_wall, p_s = timed("seq", n_leg, w_leg)
         _, p_f = timed("fused", n_leg, w_leg)
+        _, p_rm = timed("gemm_row_major", n_leg, w_leg)
         med = statistics.median
         T_G = med([p[0] for p in p_g])
         T_R = med([p[1] for p in p_r])
@@ -241,6 +246,10 @@ def main():
             "reducer_alone_GBps": rbytes / (T_R * 1e-3) / 1e9,
             "B_req_GBps": ((P - 1) / P) * M * N * 2 / (med([p[0] for p in p_f]) * 1e-3) / 1e9,
             "gemm_alone_tflops": flops / (T_G * 1e-3) / 1e12,
+            "T_gemm_row_major_ms": med([p[0] for p in p_rm]),
+            # the paper's measured communication bandwidth: the reduction's
+            # bytes over the elapsed time of the call that contains it
+            "reducer_in_fused_GBps": rbytes / (T_fused * 1e-3) / 1e9,
         }
         if layer:
             # T_fused above is the layer call; add the plain fused call and the
@@ -313,10 +322,24 @@ def main():
         "cpu_baseline": cpu,
         "overlap": legs,
         "input_gen_s": round(t_gen, 2),
+        "device": device_info(torch, M, N, cfg),
     }
     if copy:
         rec["copy_calibration"] = copy
     print(json.dumps(rec), flush=True)
+
+
+def device_info(torch, M, N, cfg):
+    """The device as the run saw it, the bf16 MFMA peak re-derived from its
+    CU count (4096 FLOP per CU per clock at the 2.4 GHz peak engine clock),
+    and the producer's wave count (blocks per CU)."""
+    p = torch.cuda.get_device_properties(0)
+    cus = int(p.multi_processor_count)
+    bm, bn = {0: (256, 256), 1: (256, 128), 2: (128, 256), 3: (128, 128)}.get(cfg.gemm_cfg, (256, 256))
+    return {"name": p.name, "arch": getattr(p, "gcnArchName", None), "cus": cus,
+            "peak_bf16_tflops_from_cus": round(cus * 4096 * 2.4e9 / 1e12, 1),
+            "peak_bf16_tflops_used": PEAK_BF16_TFLOPS,
+            "waves": round((M // bm) * (N // bn) / cus, 3)}
 
 
 def cpu_baseline(prob, w, outs, all_chunks, dest_of, lay=None):
