@@ -161,6 +161,23 @@ def test_results_independent_of_order_budget_threads_and_mode():
             assert np.array_equal(o, base[d * (M // P):(d + 1) * (M // P)]), (d, g)
 
 
+def test_zero_peers_give_the_partial_itself():
+    """With every peer zero the reduced chunk is the bf16 partial, bit for bit
+    (adding +0 in fp32 and rounding back changes nothing)."""
+    M, N, K, P = 1024, 512, 200, 4
+    print("[zero peers]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("const", 0.0), seed=77)
+    A, B, peers = upload(prob)
+    with E.Context(M, N, K, P) as ctx:
+        part = ctx.gemm_only(A, B)
+        torch.cuda.synchronize()
+        pb = host_bits(part)
+        for dest, kw in ((E.DEST_ALL, {}), (2, dict(reduce_wgs=-1)), (1, dict(launch=1)), (3, dict(launch=2))):
+            o = run(ctx, A, B, peers, dest, E.Config.make(**kw))
+            torch.cuda.synchronize()
+            assert np.array_equal(host_bits(o), pb[out_global_rows(M, P, dest)]), (dest, kw)
+
+
 def test_reducer_is_exact_on_given_partial():
     """reduce_only on a known partial equals the fp32 rank-order sum rounded
     to bf16, bit for bit; gemm_only's partial stays within the GEMM bound."""
