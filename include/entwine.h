@@ -111,15 +111,16 @@ typedef struct {
                              tiles after every g of its blocks, one release
                              each time (Section 5.3.2, release granularity:
                              every wave waits for its tile stores, plus an
-                             L2 write-back with store_mode 1); 0 = default = 1; -1 = only once,
+                             L2 write-back with store_mode 1 or 2); 0 = default = 1; -1 = only once,
                              after its last block; release groups, where a
                              tile's flag waits for its whole group:
                              -2 = its row partition (chunk), -3 = the whole
                              output (the coarse end of Section 5.3.2's
                              ablation) */
   int32_t store_mode;     /* partial tile stores: 0 = write-through (a
-                             release only waits for them), 1 = non-temporal
-                             (written back from L2 by the release) */
+                             release only waits for them), 1 = non-temporal,
+                             2 = write-back (1 and 2 are written back from
+                             L2 by each release) */
 } entwine_config;
 
 /* Fill *cfg with the defaults. */

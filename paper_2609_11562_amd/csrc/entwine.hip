@@ -137,7 +137,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   if (c.gemm_wgs < 0) return fail(ctx, ENTWINE_EINVAL, "gemm_wgs must be >= 0");
   if (c.launch < 0 || c.launch > 2) return fail(ctx, ENTWINE_EINVAL, "launch must be 0, 1 or 2");
   if (c.release_blocks < -3) return fail(ctx, ENTWINE_EINVAL, "release_blocks must be >= -3");
-  if (c.store_mode < 0 || c.store_mode > 1) return fail(ctx, ENTWINE_EINVAL, "store_mode must be 0 or 1");
+  if (c.store_mode < 0 || c.store_mode > 2) return fail(ctx, ENTWINE_EINVAL, "store_mode must be 0, 1 or 2");
   r->order = c.order;
   r->gemm_cfg = c.gemm_cfg < 0 ? default_gemm_cfg(M, N, P) : c.gemm_cfg;
   r->BM = kCfgShapes[r->gemm_cfg].BM;
@@ -294,7 +294,7 @@ GemmArgs gemm_args(entwine_ctx* ctx, const Resolved& r, const void* A, int64_t l
   g.flags = publish ? ctx->flags : nullptr;
   g.epoch = epoch;
   g.release_blocks = r.release_blocks;
-  g.nt_stores = r.store_mode;
+  g.store_mode = r.store_mode;
   g.group_ctr = ctx->group_ctr;
   g.take_ctr = nullptr;
   return g;

@@ -78,7 +78,8 @@ struct GemmArgs {
   uint32_t epoch;
   int release_blocks;     // publish after every g blocks (g >= 1), only after the last (g = -1), or
                           // by group: -2 a partition's tiles once all are stored, -3 the whole output's
-  int nt_stores;          // 1: non-temporal tile stores (written back at the release); 0: write-through
+  int store_mode;         // tile stores: 0 write-through; 1 non-temporal, 2 write-back (both written
+                          // back from L2 at the release)
   unsigned long long* group_ctr;   // release groups: tiles stored, per partition (P) then the output (1);
                                    // a multiple of the group's tile count between calls
   unsigned int* take_ctr;  // fused launch: the reduction task counter, first taken during the last epilogue
@@ -506,7 +507,8 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
         const int rr = r0 + lane / CPR, c = lane % CPR;
         const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + rr * ROWB + ((c ^ (rr % CPR)) << 4));
         uint16_t* dst = cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8;
-        if (a.nt_stores) __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(dst));
+        if (a.store_mode == 1) __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(dst));
+        else if (a.store_mode == 2) *reinterpret_cast<u32x4_t*>(dst) = v;
         else store16_wt(dst, v);
       }
       wave_sync();                               // the next round rewrites these rows
@@ -536,7 +538,7 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
       wait_vm<0>();
       __syncthreads();
       if (tid == 0) {
-        if (a.nt_stores) release_fence();
+        if (a.store_mode != 0) release_fence();
         constexpr unsigned long long c = (BM / kTile) * (BN / kTile);
         unsigned long long* ctr = a.group_ctr + (a.release_blocks == kReleasePartition ? d : a.P);
         const unsigned long long old = atomicAdd(ctr, c);
@@ -553,7 +555,7 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
       __syncthreads();
       if (tid == 0) {
         const int tiles_n = a.N / kTile;
-        if (a.nt_stores) release_fence();
+        if (a.store_mode != 0) release_fence();
         for (int pb = unpublished; pb <= lb; ++pb) {
           const BlockPos pp = pb == lb ? bp : block_of_position(a.order, w + pb * G, grid);
 #pragma unroll

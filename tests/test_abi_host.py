@@ -81,7 +81,8 @@ def test_validate_config(lib):
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=E.RELEASE_PARTITION)) == E.OK
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=E.RELEASE_OUTPUT)) == E.OK
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(release_blocks=-4)) == E.EINVAL
-    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(store_mode=2)) == E.EINVAL
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(store_mode=2)) == E.OK
+    assert E.validate(512, 1024, 256, 2, 0, E.Config.make(store_mode=3)) == E.EINVAL
     assert E.validate(512, 1024, 256, 2, 0, E.Config.make(launch=1)) == E.OK
 
 

@@ -142,7 +142,9 @@ def test_results_independent_of_order_budget_threads_and_mode():
                    [dict(release_blocks=g, launch=l, gemm_cfg=c)
                     for g in (2, E.RELEASE_AT_END, E.RELEASE_PARTITION, E.RELEASE_OUTPUT)
                     for l, c in ((0, 0), (1, 3), (2, 1))] + \
-                   [dict(release_blocks=E.RELEASE_PARTITION, reduce_wgs=-1, gemm_cfg=2)]
+                   [dict(release_blocks=E.RELEASE_PARTITION, reduce_wgs=-1, gemm_cfg=2)] + \
+                   [dict(store_mode=m, release_blocks=g, reduce_wgs=x, launch=l)
+                    for m in (1, 2) for g, x, l in ((2, -1, 0), (E.RELEASE_AT_END, 16, 0), (1, 8, 1))]
         for kw in variants:
             o = host_bits(run(ctx, A, B, peers, E.DEST_ALL, E.Config.make(**kw)))
             assert np.array_equal(o, base), kw
@@ -235,7 +237,8 @@ def test_poisoned_buffers_never_leak_across_repeated_calls():
             out.fill_(nan)
             release = (1, 2, E.RELEASE_AT_END, E.RELEASE_PARTITION, E.RELEASE_OUTPUT)[i % 5]
             ctx.gemm_rs(A, B, peers, 5, out=out, partial=partial, reduce_stream=rs,
-                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 3, release_blocks=release))
+                        cfg=E.Config.make(reduce_wgs=8 + i, launch=(i // 2) % 3, release_blocks=release,
+                                          store_mode=(i // 6) % 3))
             got = host_bits(out)
             if i < 2:
                 check_rows(probs[i], got, out_global_rows(M, P, 5))
