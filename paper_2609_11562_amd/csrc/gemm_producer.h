@@ -484,7 +484,11 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
     // time are staged in this wave's own LDS area (16-byte chunks
     // XOR-swizzled by row), then stored as whole rows with 16-byte lanes, so
     // every store instruction writes full 128-byte lines.
+    // The store mode is chosen once per block, so the unrolled stores carry
+    // no per-store branch.
     uint16_t* cblk = a.C + static_cast<int64_t>(bp.mb * BM + wm * S::WM) * a.ldc + bp.nb * BN + wn * S::WN;
+    auto epilogue = [&](auto mode) {
+      constexpr int SM = decltype(mode)::value;
 #pragma unroll
     for (int i = 0; i < S::FM; ++i) {
       const int r = lane & 31;
@@ -507,12 +511,16 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
         const int rr = r0 + lane / CPR, c = lane % CPR;
         const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cst + rr * ROWB + ((c ^ (rr % CPR)) << 4));
         uint16_t* dst = cblk + static_cast<int64_t>(i * 32 + rr) * a.ldc + c * 8;
-        if (a.store_mode == 1) __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(dst));
-        else if (a.store_mode == 2) *reinterpret_cast<u32x4_t*>(dst) = v;
+        if (SM == 1) __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(dst));
+        else if (SM == 2) *reinterpret_cast<u32x4_t*>(dst) = v;
         else store16_wt(dst, v);
       }
       wave_sync();                               // the next round rewrites these rows
     }
+    };
+    if (a.store_mode == 1) epilogue(IC<1>{});
+    else if (a.store_mode == 2) epilogue(IC<2>{});
+    else epilogue(IC<0>{});
 
     // Release granularity (paper Section 5.3.2): one release covers the
     // tiles of every block since the last publication.  With release groups
