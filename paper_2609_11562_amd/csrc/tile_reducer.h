@@ -229,9 +229,9 @@ __device__ __forceinline__ void reducer_body(const ReduceArgs& a, const int j, i
   }
 }
 
-// Publishes, as part of one launch, the synthetic peers' flags of every tile
-// the call reduces (a.call_tiles),
-// split over all nb workgroups; peer `withhold_peer` stays unpublished.
+// Publishes, as part of one launch, the synthetic peers' flags of the
+// a.call_tiles tiles the call reduces, split over all nb workgroups; peer
+// `withhold_peer` stays unpublished.
 __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, int b, int nb) {
   const BlockGrid grid = make_grid(a.M, a.N, np, a.BM, a.BN, a.group_m);
   const int tiles_n = a.N / kTile;
@@ -250,13 +250,14 @@ __device__ __forceinline__ void publish_peer_slice(const ReduceArgs& a, int np, 
   }
 }
 
-// The reducer role with dynamic tasks: workgroups take half-tiles from a
-// device counter in consumer order (task t is half t % 2 of tile u = t / 2
-// of the destination's partition; with every destination, tile u / P of
-// partition u % P, which interleaves the partitions as Equation 1 does), so
-// the dedicated reducers and every producer that has finished its blocks
-// share the remaining work; half-tiles keep every workgroup busy when a
-// chunk has fewer tiles than the device has CUs.
+// The reducer role with dynamic tasks: workgroups take tile parts (SPLIT per
+// tile, kTaskSplit in the fused launch) from a device counter in consumer
+// order (task t is part t % SPLIT of tile u = t / SPLIT of the destination's
+// partition; with every destination, tile u / P of partition u % P, which
+// interleaves the partitions as Equation 1 does), so the dedicated reducers
+// and every producer that has finished its blocks share the remaining work;
+// parts keep every workgroup busy when a chunk has fewer tiles than the
+// device has CUs.  `taken`, if not ~0u, is the first task, already taken.
 // Each workgroup ends with one failed take; the last workgroup of the grid to
 // finish returns both counters to zero, ready for the next call.  After a
 // timeout waits are skipped (the call's output is then undefined) but the
