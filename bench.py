@@ -220,6 +220,19 @@ def main():
     algo_bytes = 2.0 * (M * K + K * N + M * N) + 2.0 * rows_out * N * (P + 1)
     if layer and main_mode == "fused":
         algo_bytes += 2.0 * rows_out * N * 3     # residual read, h and y written
+    # The call's bound is whichever of its flops at the MFMA peak and its
+    # algorithmic bytes at the HBM peak takes longer (the rank share of the
+    # LLM shapes is MFMA-bound; every chunk of a short-K shape is HBM-bound).
+    hbm_bound = algo_bytes / (PEAK_HBM_GBPS * 1e9) > flops / (PEAK_BF16_TFLOPS * 1e12)
+    if hbm_bound:
+        ach = algo_bytes / (mean_k * 1e-3) / 1e9 if mean_k else None
+        roof = {"bound": "hbm", "kernel": kernel, "achieved": round(ach, 1) if ach else None,
+                "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
+                "achieved_tflops": round(achieved, 2) if achieved else None}
+    else:
+        roof = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2) if achieved else None,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None}
 
     legs = {}
     if not args.no_legs and args.only is None:
@@ -309,10 +322,7 @@ def main():
                    "reduce_threads": cfg.reduce_threads, "group_m": cfg.group_m, "gemm_wgs": cfg.gemm_wgs,
                    "launch": cfg.launch, "release_blocks": cfg.release_blocks,
                    "epilogue": "residual + RMSNorm" if layer else None},
-        "roofline": {"bound": "mfma", "kernel": kernel,
-                     "achieved": round(achieved, 2) if achieved else None,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
+        "roofline": {**roof,
                      "traffic": traffic["bytes"] if traffic else None,
                      "traffic_detail": traffic,
                      "algorithmic_bytes": round(algo_bytes),
