@@ -180,6 +180,23 @@ def test_zero_peers_give_the_partial_itself():
             assert np.array_equal(host_bits(o), pb[out_global_rows(M, P, dest)]), (dest, kw)
 
 
+def test_every_budget_up_to_the_cap_completes_and_agrees():
+    """No budget x from 1 to past the cap hangs or changes a bit, in any fused
+    form (the library clamps x to min(tiles per chunk, CUs - 1))."""
+    M, N, K, P = 4096, 2048, 64, 4
+    print("[budgets]", flush=True)
+    prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.01), seed=88)
+    A, B, peers = upload(prob)
+    with E.Context(M, N, K, P) as ctx:
+        base = host_bits(run(ctx, A, B, peers, 1))
+        torch.cuda.synchronize()
+        check_rows(prob, base[::61], out_global_rows(M, P, 1)[::61])
+        for launch in (0, 1, 2):
+            for x in (1, 2, 3, 7, 31, 64, 127, 128, 200, 255):
+                o = host_bits(run(ctx, A, B, peers, 1, E.Config.make(launch=launch, reduce_wgs=x, timeout_us=500000)))
+                assert np.array_equal(o, base), (launch, x)
+
+
 def test_reducer_is_exact_on_given_partial():
     """reduce_only on a known partial equals the fp32 rank-order sum rounded
     to bf16, bit for bit; gemm_only's partial stays within the GEMM bound."""
