@@ -76,12 +76,16 @@ typedef struct {
   int32_t order;          /* entwine_order (default INTERLEAVED) */
   int32_t gemm_cfg;       /* entwine_gemm_cfg, -1 = largest that divides */
   int32_t reduce_wgs;     /* x: reducer grid size, the communication budget
-                             (Section 3.2); 0 = default; capped at the tile
-                             count and at CUs - 1.  With DEST_ALL it is
-                             rounded up to a multiple of P.  With launch 0,
-                             producers that finish their blocks also take
-                             tiles, and -1 asks for no dedicated reducers
-                             at all (all CUs produce, then reduce). */
+                             (Section 3.2); capped at the tile count and at
+                             CUs - 1.  With DEST_ALL it is rounded up to a
+                             multiple of P.  With launch 0, producers that
+                             finish their blocks also take tiles, and -1
+                             asks for no dedicated reducers at all (all CUs
+                             produce, then reduce).  0 = default: none with
+                             launch 0, 16 with launch 1, one per CU with
+                             launch 2; the standalone reducer
+                             (entwine_reduce_only and the sequential form)
+                             then uses 16. */
   int32_t reduce_threads; /* b: threads per reducer workgroup, 128/256/512/1024
                              (0 = default = 1024) */
   int32_t timeout_us;     /* bound on one reducer wait, microseconds
@@ -111,7 +115,7 @@ typedef struct {
                              tiles after every g of its blocks, one release
                              each time (Section 5.3.2, release granularity:
                              every wave waits for its tile stores, plus an
-                             L2 write-back with store_mode 1 or 2); 0 = default = 1; -1 = only once,
+                             L2 write-back with store_mode 1 or 2); 0 = default = 2; -1 = only once,
                              after its last block; release groups, where a
                              tile's flag waits for its whole group:
                              -2 = its row partition (chunk), -3 = the whole

@@ -158,7 +158,9 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
     x = std::min(std::min(x, Q), cap_cus);
   }
   r->x_alone = std::max(x, 1);
-  r->x = c.reduce_wgs == -1 ? 0 : r->x_alone;
+  // The single launch defaults to no dedicated reducers: producers reduce
+  // once their blocks are done, which measured fastest on most shapes.
+  r->x = c.reduce_wgs == -1 || (c.reduce_wgs == 0 && c.launch == 0) ? 0 : r->x_alone;
   r->threads = c.reduce_threads ? c.reduce_threads : 1024;
   r->withhold = c.withhold_peer;
   r->timing = c.record_timing;
@@ -166,7 +168,7 @@ entwine_status resolve(entwine_ctx* ctx, int64_t M, int64_t N, int32_t P, int32_
   r->group_m = c.group_m ? c.group_m : 4;
   r->gemm_wgs = c.gemm_wgs;
   r->launch = c.launch;
-  r->release_blocks = c.release_blocks == 0 ? 1 : c.release_blocks;   // -1: at the end; -2, -3: groups
+  r->release_blocks = c.release_blocks == 0 ? 2 : c.release_blocks;   // -1: at the end; -2, -3: groups
   r->store_mode = c.store_mode;
   return ENTWINE_OK;
 }
