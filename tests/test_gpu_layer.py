@@ -93,7 +93,8 @@ def test_layer_invariant_across_configs_and_repeated_calls():
     y = torch.empty(rows, N, dtype=torch.bfloat16, device="cuda")
     rs = torch.cuda.Stream()
     cfgs = [None, dict(group_m=1), dict(gemm_cfg=3), dict(reduce_wgs=16), dict(reduce_wgs=-1, release_blocks=-1),
-            dict(gemm_cfg=2, release_blocks=2), None]
+            dict(gemm_cfg=2, release_blocks=2), dict(release_blocks=E.RELEASE_PARTITION, reduce_wgs=8),
+            dict(release_blocks=E.RELEASE_OUTPUT, store_mode=2), dict(store_mode=1, order=E.ORDER_M_MAJOR), None]
     with E.Context(M, N, K, P) as ctx:
         base = None
         for i, kw in enumerate(cfgs):
@@ -136,6 +137,23 @@ def test_layer_full_size_sampled_rows(name):
                 hb, yb = host_bits(h[sel]), host_bits(y[sel])
                 grow = out_rows(w.M, w.P, dest)[lrow]
                 check_layer(prob, R[lrow], gamma, hb, yb, grow, np.arange(len(lrow)))
+    del A, B, peers
+    torch.cuda.empty_cache()
+
+
+def test_layer_full_size_every_chunk_sampled_rows():
+    """All chunks at once (M row tasks) at the 4K-token layer shape."""
+    w = WORKLOADS["llama70b_attn_out_layer_seq4k_tp8"]
+    print(f"[layer full all-chunks {w.name}]", flush=True)
+    prob = w.problem()
+    A, B, peers = dev(prob.A), dev(prob.B), [dev(p) for p in prob.peers]
+    R, gamma = make_layer_inputs(w.M, w.N, 61)
+    with E.Context(w.M, w.N, w.K, w.P) as ctx:
+        h, y = ctx.gemm_rs_rmsnorm(A, B, peers, E.DEST_ALL, dev(R), dev(gamma), EPS)
+        assert ctx.query_status()[0] == E.OK
+        lrow = np.array([0, 127, 511, 512, 1500, 2047, 2048, 3333, 4095])
+        sel = torch.as_tensor(lrow, device="cuda")
+        check_layer(prob, R[lrow], gamma, host_bits(h[sel]), host_bits(y[sel]), lrow, np.arange(len(lrow)))
     del A, B, peers
     torch.cuda.empty_cache()
 
