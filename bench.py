@@ -198,6 +198,11 @@ def main():
 
     main_mode = args.only or "fused"
     ms_per_step, per = timed(main_mode, args.steps, args.warmup)
+    # Engine clock of the producer role over the timed single-launch calls
+    # (engine cycles over wall-clock time, from the workgroups' own stamps).
+    clock_ghz = None
+    if main_mode in ("fused", "plain") and cfg.launch == 0:
+        clock_ghz = statistics.median(ctx.last_clock(b) for b in range(min(args.steps, 255)))
     g_ms = [p[0] for p in per if p[0] > 0]
     r_ms = [p[1] for p in per if p[1] > 0]
     e_ms = [p[2] for p in per if p[2] > 0]
@@ -233,6 +238,12 @@ def main():
         roof = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2) if achieved else None,
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None}
+        if clock_ghz and achieved:
+            # the MFMA peak at the clock the producer actually ran at
+            cus = torch.cuda.get_device_properties(0).multi_processor_count
+            peak_clk = cus * 4096 * clock_ghz * 1e9 / 1e12
+            roof.update({"clock_ghz": round(clock_ghz, 3), "peak_at_clock": round(peak_clk, 1),
+                         "frac_at_clock": round(achieved / peak_clk, 4)})
 
     legs = {}
     if not args.no_legs and args.only is None:

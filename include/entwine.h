@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define ENTWINE_ABI_VERSION 2
+#define ENTWINE_ABI_VERSION 3
 #define ENTWINE_TILE 128      /* side of a reduction tile (Section 4.2) */
 #define ENTWINE_MAX_P 8       /* chunk count supported (the paper's W <= 8) */
 #define ENTWINE_DEST_ALL (-1) /* reduce every chunk (one-GPU emulation) */
@@ -209,6 +209,17 @@ entwine_status entwine_reduce_only(entwine_ctx* ctx, const void* partial, int64_
  * than 1024 workgroups).  Blocks until the call completes. */
 entwine_status entwine_last_stamps(entwine_ctx* ctx, int32_t back, uint64_t* stamps, int32_t capacity,
                                    int32_t* nwgs, int32_t* nproducers, double* ticks_per_us);
+
+/* Engine clock of the producer role during the `back`-th most recent
+ * single-launch call made with record_timing: the engine cycles the producer
+ * workgroups counted (s_memtime) over the wall-clock time they spanned,
+ * summed over those workgroups, in GHz (host double written to *ghz; 0 if no
+ * workgroup produced).  The MFMA peak scales with this clock, which sits
+ * below the 2.4 GHz maximum under sustained matrix load and depends on the
+ * operand data (Section 5's throughput figures are at whatever clock the
+ * device held).  ENTWINE_EUNSUPPORTED for a call without stamps (as for
+ * entwine_last_stamps).  Blocks until the call completes. */
+entwine_status entwine_last_clock(entwine_ctx* ctx, int32_t back, double* ghz);
 
 /* Waits for the context's queued work, then reports the device status word:
  * returns ENTWINE_ETIMEOUT (with the tile and the flag source, -1 = local,

@@ -25,6 +25,11 @@ ablations (Section 5.3):
               Table 1, each with its GEMM wave count (256 x 256 producer
               blocks per CU), the single launch at its best budget and the
               non-overlapped baseline.
+* ``clock``   what bounds the producer on this device: the single launch on
+              the three LLM shapes with the seeded operands, with A = 0 and
+              with A = B = 1 (the same instructions, cycles and bytes; only
+              the switching activity of the matrix cores differs), each with
+              the engine clock the producers ran at.
 
 M = N = 8192 and P = 8 throughout, except in ``range``.  Every row reports the wall-clock latency
 per call (median over rounds of ``steps`` calls), the producer's window and
@@ -93,7 +98,7 @@ class Bench:
             self.ctx.gemm_rs(self.A, self.B, self.peers, i % w.P, out=self.out, partial=self.partial, cfg=cfg,
                              gemm_stream=self.gs, reduce_stream=rs)
 
-        walls, gemm, e2e = [], [], []
+        walls, gemm, e2e, clk = [], [], [], []
         for _ in range(self.rounds):
             for i in range(self.warmup):
                 call(i)
@@ -110,10 +115,15 @@ class Bench:
                 g, _, e = self.ctx.last_timing(b)
                 gemm.append(g)
                 e2e.append(e)
+                if cfg.launch == 0:
+                    clk.append(self.ctx.last_clock(b))
         T = statistics.median(walls)
         G, Ee = statistics.median(gemm), statistics.median(e2e)
-        return {"ms": round(T, 5), "gemm_window_ms": round(G, 5), "e2e_event_ms": round(Ee, 5),
-                "tail_ms": round(max(0.0, Ee - G), 5), "tflops": round(w.flops / (T * 1e-3) / 1e12, 1)}
+        out = {"ms": round(T, 5), "gemm_window_ms": round(G, 5), "e2e_event_ms": round(Ee, 5),
+               "tail_ms": round(max(0.0, Ee - G), 5), "tflops": round(w.flops / (T * 1e-3) / 1e12, 1)}
+        if clk:
+            out["clock_ghz"] = round(statistics.median(clk), 3)
+        return out
 
 
 def best_over_budgets(bench: Bench, budgets, **kw):
@@ -202,7 +212,27 @@ def study_range(ks, budgets, emit, **tk):
             b.close()
 
 
-STUDIES = {"order": (study_order, (512, 2048)), "pool": (study_pool, (512, 2048)), "range": (study_range, ()),
+def study_clock(ks, budgets, emit, **tk):
+    """ks, budgets: unused (the LLM shapes and the default single launch)."""
+    del ks, budgets
+    for name in ("llama7b_mlp_down_tp8", "llama70b_attn_out_tp8", "llama70b_mlp_down_tp8"):
+        b = Bench(WORKLOADS[name], **tk)
+        A0, B0 = b.A.clone(), b.B.clone()
+        for data in ("seeded", "a_zero", "ones", "seeded"):
+            b.A.copy_(A0)
+            b.B.copy_(B0)
+            if data == "a_zero":
+                b.A.zero_()
+            elif data == "ones":
+                b.A.fill_(1.0)
+                b.B.fill_(1.0)
+            r = b.time(launch=0)
+            emit({"study": "clock", "workload": name, "data": data, **r})
+        del A0, B0
+        b.close()
+
+
+STUDIES = {"clock": (study_clock, ()), "order": (study_order, (512, 2048)), "pool": (study_pool, (512, 2048)), "range": (study_range, ()),
            "release": (study_release, (2048, 4096, 8192)),
            "budget": (study_budget, (256, 512, 768, 1024, 1536, 2048, 3072, 4096))}
 

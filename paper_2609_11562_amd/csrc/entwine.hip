@@ -740,6 +740,15 @@ entwine_status entwine_query_status(entwine_ctx* ctx, int32_t* code, int32_t* ti
   return ENTWINE_OK;
 }
 
+// The per-workgroup stamps of a single-launch call, once it has completed.
+static entwine_status read_stamps(entwine_ctx* ctx, const TimingSlot& s, std::vector<unsigned long long>& h) {
+  HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
+  h.resize(size_t(s.grid) * kStampsPerWg);
+  HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * kStampsPerWg,
+                             h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+  return ENTWINE_OK;
+}
+
 entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_ms, float* reduce_ms,
                                    float* e2e_ms) {
   if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
@@ -751,9 +760,8 @@ entwine_status entwine_last_timing(entwine_ctx* ctx, int32_t back, float* gemm_m
     // from the first workgroup's start; end to end from the events around it.
     HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
     HIP_OR_FAIL(ctx, hipEventElapsedTime(&e, s.start, s.red_end));
-    std::vector<unsigned long long> h(size_t(s.grid) * kStampsPerWg);
-    HIP_OR_FAIL(ctx, hipMemcpy(h.data(), ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * kStampsPerWg,
-                               h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    std::vector<unsigned long long> h;
+    CHECK(read_stamps(ctx, s, h));
     unsigned long long t0 = ~0ull, ge = 0, re = 0;
     for (int b = 0; b < s.grid; ++b) {
       t0 = std::min(t0, h[kStampsPerWg * b]);
@@ -793,10 +801,31 @@ entwine_status entwine_last_stamps(entwine_ctx* ctx, int32_t back, uint64_t* sta
   if (nproducers) *nproducers = s.G;
   if (ticks_per_us) *ticks_per_us = double(ctx->ticks_per_us);
   if (!stamps) return ENTWINE_OK;
-  if (capacity < s.grid * kStampsPerWg) return fail(ctx, ENTWINE_EINVAL, "capacity below %d", s.grid * kStampsPerWg);
-  HIP_OR_FAIL(ctx, hipEventSynchronize(s.red_end));
-  HIP_OR_FAIL(ctx, hipMemcpy(stamps, ctx->stamps + size_t(&s - ctx->ring) * kStampWgs * kStampsPerWg,
-                             size_t(s.grid) * kStampsPerWg * sizeof(uint64_t), hipMemcpyDeviceToHost));
+  if (capacity < s.grid * 4) return fail(ctx, ENTWINE_EINVAL, "capacity below %d", s.grid * 4);
+  std::vector<unsigned long long> h;
+  CHECK(read_stamps(ctx, s, h));
+  for (int b = 0; b < s.grid; ++b)
+    for (int i = 0; i < 4; ++i) stamps[4 * b + i] = h[size_t(kStampsPerWg) * b + i];
+  return ENTWINE_OK;
+}
+
+entwine_status entwine_last_clock(entwine_ctx* ctx, int32_t back, double* ghz) {
+  if (!ctx) return fail(nullptr, ENTWINE_EINVAL, "ctx is NULL");
+  if (!ghz) return fail(ctx, ENTWINE_EINVAL, "ghz is NULL");
+  if (back < 0 || back >= kRing || back >= ctx->ncalls) return fail(ctx, ENTWINE_EINVAL, "no such timed call");
+  const TimingSlot& s = ctx->ring[(ctx->ncalls - 1 - back) % kRing];
+  if (!s.has_stamps) return fail(ctx, ENTWINE_EUNSUPPORTED, "the call has no workgroup timestamps");
+  std::vector<unsigned long long> h;
+  CHECK(read_stamps(ctx, s, h));
+  // Cycles over wall-clock time, summed over the producer workgroups.
+  double cycles = 0.0, ticks = 0.0;
+  for (int b = 0; b < s.G; ++b) {
+    const unsigned long long* t = h.data() + size_t(kStampsPerWg) * b;
+    if (t[1] <= t[0] || t[5] <= t[4]) continue;
+    cycles += double(t[5] - t[4]);
+    ticks += double(t[1] - t[0]);
+  }
+  *ghz = ticks > 0.0 ? cycles / (ticks / double(ctx->ticks_per_us)) / 1e3 : 0.0;
   return ENTWINE_OK;
 }
 

@@ -21,20 +21,35 @@
 
 namespace entwine {
 
-constexpr int kStampsPerWg = 4;
+constexpr int kStampsPerWg = 6;
 
-// stamps: null, or kStampsPerWg per workgroup in wall-clock ticks: {start,
-// producer end (= start without producer work), first reduction task ready
-// (0 if none), end}.
+// stamps: null, or kStampsPerWg per workgroup: {start, producer end (= start
+// without producer work), first reduction task ready (0 if none), end} in
+// wall-clock ticks, then the engine clock's cycle counter at the start and at
+// the producer end, which over the wall-clock span give the clock the
+// producer ran at (it falls under load, and depends on the data).
 template <int BM, int BN, bool TAIL>
 __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs r, int G, int np,
                                                           unsigned long long* stamps) {
   __shared__ __attribute__((aligned(1024))) char smem[GemmShape<BM, BN>::LDS_BYTES];
-  const unsigned long long t0 = stamps ? wall_clock64() : 0;
   const int b = blockIdx.x;
+  // Stamps are stored as they are taken, so none stays live in registers
+  // across the producer.
+  unsigned long long* const st = stamps && threadIdx.x == 0 ? stamps + kStampsPerWg * b : nullptr;
+  if (st) {
+    st[0] = wall_clock64();
+    st[4] = __builtin_amdgcn_s_memtime();
+    if (b >= G) {
+      st[1] = st[0];
+      st[5] = st[4];
+    }
+  }
   publish_peer_slice(r, np, b, gridDim.x);
   const unsigned int taken = b < G ? producer_body<BM, BN, TAIL>(g, b, G, smem) : ~0u;
-  const unsigned long long t1 = stamps ? wall_clock64() : 0;
+  if (st && b < G) {
+    st[1] = wall_clock64();
+    st[5] = __builtin_amdgcn_s_memtime();
+  }
   int* s = reinterpret_cast<int*>(smem);
   static_assert(kLayerThreads == 256, "the layer tasks run on the fused launch's workgroups");
   if (r.layer) {
@@ -63,11 +78,9 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   }
   if (stamps) {
     __syncthreads();
-    if (threadIdx.x == 0) {
-      stamps[kStampsPerWg * b] = t0;
-      stamps[kStampsPerWg * b + 1] = b < G ? t1 : t0;
-      if (r.layer) stamps[kStampsPerWg * b + 2] = 0;
-      stamps[kStampsPerWg * b + 3] = wall_clock64();
+    if (st) {
+      if (r.layer) st[2] = 0;
+      st[3] = wall_clock64();
     }
   }
 }

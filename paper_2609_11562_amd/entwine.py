@@ -72,6 +72,7 @@ _PROTOS = {
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
     "entwine_last_stamps": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_uint64), _i32, _P32, _P32,
                                    ctypes.POINTER(ctypes.c_double)]),
+    "entwine_last_clock": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_double)]),
     "entwine_validate": (_i32, [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(Config)]),
     "entwine_tile_schedule": (_i32, [_i32, _i64, _i64, _i32, _i32, _i32, _i32, _P32, _P32]),
     "entwine_consumer_tasks": (_i32, [_i32, _i32, _i32, _i32, _i32, _P32, _P32, _i32, _P32]),
@@ -291,6 +292,13 @@ class Context:
         us = (raw.astype(np.float64) - float(t0)) / tpu.value
         us[raw[:, 2] == 0, 2] = np.nan
         return us, g.value
+
+    def last_clock(self, back: int = 0) -> float:
+        """Engine clock (GHz) the producer role ran at during a single-launch
+        call made with record_timing=1."""
+        ghz = ctypes.c_double()
+        _check(lib().entwine_last_clock(self._h, back, ctypes.byref(ghz)), self._h)
+        return ghz.value
 
     def last_timing(self, back: int = 0):
         """(gemm_ms, reduce_ms, e2e_ms) of a call made with record_timing=1."""

@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_strings(lib):
-    assert lib.entwine_abi_version() == 2
+    assert lib.entwine_abi_version() == 3
     assert ctypes.sizeof(E.Config) == 12 * 4
     assert E._status_name(E.ETIMEOUT) == "ENTWINE_ETIMEOUT"
     c = E.Config.make()

@@ -317,7 +317,12 @@ def test_workgroup_timeline_is_consistent(tiny):
     ready = ~np.isnan(us[:, 2])
     assert ready.any() and np.all(us[ready, 2] >= us[ready, 1]) and np.all(us[ready, 2] <= us[ready, 3])
     assert np.all(us[G:, 1] == us[G:, 0])   # dedicated reducers have no producer role
+    # the engine clock the producers ran at: above 0.1 GHz, at most the
+    # 2.4 GHz maximum (with a margin for counter granularity on a tiny call)
+    ghz = ctx.last_clock()
+    assert 0.1 < ghz < 2.6, ghz
     run(ctx, A, B, peers, 1, E.Config.make(record_timing=1, launch=1))
-    with pytest.raises(E.EntwineError) as ei:
-        ctx.last_stamps()
-    assert ei.value.status == E.EUNSUPPORTED
+    for query in (ctx.last_stamps, ctx.last_clock):
+        with pytest.raises(E.EntwineError) as ei:
+            query()
+        assert ei.value.status == E.EUNSUPPORTED

@@ -40,7 +40,7 @@ def test_write_entry_round_trip(tmp_path):
 
 def test_ablation_studies_and_shapes():
     from paper_2609_11562_amd import ablation
-    assert set(ablation.STUDIES) == {"order", "pool", "release", "budget", "range"}
+    assert set(ablation.STUDIES) == {"order", "pool", "release", "budget", "range", "clock"}
     assert len(ablation.STUDIES["budget"][1]) == 8
     for K in (512, 768, 4096):
         w = ablation.workload(K)
