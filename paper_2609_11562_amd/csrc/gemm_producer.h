@@ -26,7 +26,7 @@
 //  * LDS layouts are chosen for conflict-free operand reads, and realised by
 //    permuting which global 16-byte chunk each lane fetches:
 //      A stage: [BM rows][32 k] (64-byte rows), chunk c of row r stored at
-//               chunk c ^ (((r >> 1) ^ (r >> 3)) & 3);
+//               chunk c ^ a_swizzle(r) (below);
 //      B stage: [32 k][BN n] (row-major, as in memory), chunk c of row k
 //               stored at chunk c ^ (4 (k & 3)).
 //  * A operands: one ds_read_b128 per 32 x 16 fragment (8 consecutive k per
@@ -155,6 +155,16 @@ __device__ __forceinline__ void dma16_s(const void* base, uint32_t off, uint32_t
                : "memory");
 }
 
+// 16-byte chunk permutation of A stage row r.  An A fragment read
+// (ds_read_b128) puts lanes 0-31 (and 32-63) on 32 consecutive rows at one
+// logical chunk.  On gfx950 the LDS bank-conflict counter (a probe of this
+// exact pattern) reads zero for XOR masks (r >> 2) & 3, (r >> 3) & 3 and
+// (r ^ (r >> 2)) & 3, and 2-way conflicts for ((r >> 1) ^ (r >> 3)) & 3,
+// (r >> 1) & 3 and ((r >> 2) ^ (r >> 4)) & 3 (4-way unpermuted).
+// (r ^ (r >> 2)) & 3 is the one of the three that is also conflict-free in
+// the textbook bank models (8 lanes over 32 banks, 16 lanes over 64).
+__device__ __forceinline__ int a_swizzle(int r) { return (r ^ (r >> 2)) & 3; }
+
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -255,7 +265,7 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
 #pragma unroll
   for (int i = 0; i < S::A_DMA; ++i) {
     const int r = (wave * S::A_DMA + i) * 16 + (lane >> 2);
-    const int lc = (lane & 3) ^ (((r >> 1) ^ (r >> 3)) & 3);
+    const int lc = (lane & 3) ^ a_swizzle(r);
     a_off[i] = static_cast<uint32_t>((r * a.lda + lc * 8) * 2);
     a_k[i] = lc * 8;
   }
@@ -346,7 +356,7 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
   // A fragment i of K-step q: rows wm*WM + 32 i + lane % 32, 8 consecutive k
   // at 16 q + 8 (lane / 32), i.e. logical chunk 2 q + lane / 32.
   const int a_row = wm * S::WM + (lane & 31);
-  const int a_sw = ((a_row >> 1) ^ (a_row >> 3)) & 3;    // same for a_row + 32 i
+  const int a_sw = a_swizzle(a_row);                      // same for a_row + 32 i
   int a_rd[S::Q];
 #pragma unroll
   for (int q = 0; q < S::Q; ++q) a_rd[q] = a_row * S::A_ROW + (((2 * q + (lane >> 5)) ^ a_sw) << 4);
