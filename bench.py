@@ -209,6 +209,20 @@ def main():
 
     flops = 2.0 * M * N * K
     value = flops / (ms_per_step * 1e-3) / 1e12
+    # Each step emulates one rank (its destination chunk); in a real TP step
+    # every rank runs at once and the step takes the slowest rank's time.
+    # Per-rank medians of the timed calls' event times (newest call first).
+    ranks = None
+    if dest_mode == "cycle" and e_ms and len(per) >= 2 * P:
+        by_rank = {}
+        for back, p in enumerate(per):
+            if p[2] > 0:
+                by_rank.setdefault(dest_of(args.steps - 1 - back), []).append(p[2])
+        med_r = {d: statistics.median(v) for d, v in sorted(by_rank.items())}
+        worst = max(med_r.values())
+        ranks = {"per_rank_ms": [round(med_r[d], 5) for d in sorted(med_r)], "max_ms": round(worst, 5),
+                 "min_ms": round(min(med_r.values()), 5),
+                 "tflops_at_max": round(flops / (worst * 1e-3) / 1e12, 2)}
     mean_g = statistics.fmean(g_ms) if g_ms else None
     # Dominant kernel: the single fused launch (both roles) when the path runs
     # as one kernel, else the producer.  Its mean duration comes from HIP
@@ -229,7 +243,20 @@ def main():
     # algorithmic bytes at the HBM peak takes longer (the rank share of the
     # LLM shapes is MFMA-bound; every chunk of a short-K shape is HBM-bound).
     hbm_bound = algo_bytes / (PEAK_HBM_GBPS * 1e9) > flops / (PEAK_BF16_TFLOPS * 1e12)
-    if hbm_bound:
+    if main_mode == "reduce":
+        # --only reduce: the standalone reducer kernel, HBM-bound; its bytes
+        # are the P contributions read and the chunk written.
+        r_ms_all = [p[1] for p in per if p[1] > 0]
+        mean_k = statistics.fmean(r_ms_all) if r_ms_all else None
+        kernel = "tile_reducer"
+        algo_bytes = 2.0 * rows_out * N * (P + 1)
+        ach = algo_bytes / (mean_k * 1e-3) / 1e9 if mean_k else None
+        roof = {"bound": "hbm", "kernel": kernel, "achieved": round(ach, 1) if ach else None,
+                "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
+                "note": "event span of the reducer launch, which also covers the queueing behind the two "
+                        "flag-publication kernels launched before it; rocprofv3's kernel duration is the "
+                        "reducer alone"}
+    elif hbm_bound:
         ach = algo_bytes / (mean_k * 1e-3) / 1e9 if mean_k else None
         roof = {"bound": "hbm", "kernel": kernel, "achieved": round(ach, 1) if ach else None,
                 "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
@@ -342,6 +369,7 @@ def main():
                      "producer_tflops": round(flops / (mean_g * 1e-3) / 1e12, 2) if mean_g else None},
         "cpu_baseline": cpu,
         "overlap": legs,
+        "ranks": ranks,
         "input_gen_s": round(t_gen, 2),
         "device": device_info(torch, M, N, cfg),
     }
