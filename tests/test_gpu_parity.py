@@ -307,6 +307,29 @@ def test_full_size_workloads_on_sampled_rows(name):
     torch.cuda.empty_cache()
 
 
+def test_sweep_orders_and_budgets_full_size():
+    """The schedule / CU-split sweep at full size (M = N = 8192, K = 2048,
+    P = 8): row-major against chunk-interleaved order, reducer budgets 4 and
+    32, single launch and two streams, on sampled rows of one chunk and of
+    every chunk."""
+    w = WORKLOADS["sweep_8192x2048x8192_p8"]
+    print("[full sweep]", flush=True)
+    prob = w.problem()
+    A, B, peers = upload(prob)
+    with E.Context(w.M, w.N, w.K, w.P) as ctx:
+        for order in (E.ORDER_INTERLEAVED, E.ORDER_ROW_MAJOR):
+            for x in (4, 32):
+                for launch in (0, 1):
+                    for dest in (3, E.DEST_ALL):
+                        o = run(ctx, A, B, peers, dest, E.Config.make(order=order, reduce_wgs=x, launch=launch))
+                        torch.cuda.synchronize()
+                        grow = sample_rows(w.M, w.P, dest, n=12, seed=x + launch)
+                        local = grow - (0 if dest == E.DEST_ALL else dest * (w.M // w.P))
+                        check_rows(prob, host_bits(o[torch.as_tensor(local, device="cuda")]), grow)
+    del A, B, peers
+    torch.cuda.empty_cache()
+
+
 def test_workgroup_timeline_is_consistent(tiny):
     w, prob, ctx, (A, B, peers) = tiny
     print("[stamps]", flush=True)
