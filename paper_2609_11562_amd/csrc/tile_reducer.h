@@ -378,139 +378,185 @@ __device__ __forceinline__ bool wave_await_row(const ReduceArgs& a, int tr, int 
   return true;
 }
 
-// Output row `orow` of the call (a row of `out`): h, its sum of squares, y.
-// `red` is kLayerThreads / 64 floats of LDS.
-template <int NP, typename Hook>
-__device__ __forceinline__ void layer_row(const ReduceArgs& a, int64_t orow, float* red, Hook after_first_loads) {
-  constexpr int B = 4;   // steps per batch: (NP + 1) x 4 loads in flight per lane
-  static_assert(kLayerMaxSteps % B == 0, "batches tile the steps");
+// Loads of one batch of output row `orow` (kLayerBatch steps of 2048
+// columns from step s0): this thread's 16 bytes of the local contribution, of
+// every peer and of the residual, per step.
+constexpr int kLayerBatch = 4;
+static_assert(kLayerMaxSteps % kLayerBatch == 0, "batches tile the steps");
+
+template <int NP>
+struct LayerLoads {
+  r_u32x4_t lv[kLayerBatch], rv[kLayerBatch];
+  r_u32x4_t pv[NP > 1 ? NP - 1 : 1][kLayerBatch];
+};
+
+template <int NP>
+__device__ __forceinline__ void layer_issue(const ReduceArgs& a, int64_t orow, int s0, LayerLoads<NP>& L) {
   const int64_t grow = orow + (a.dest >= 0 ? static_cast<int64_t>(a.dest) * (a.M / NP) : 0);
   const int c0 = threadIdx.x * 8;
-  const int steps = (a.N + kLayerCols - 1) / kLayerCols;
-  r_u32x4_t h[kLayerMaxSteps];
+#pragma unroll
+  for (int b = 0; b < kLayerBatch; ++b) {
+    const int c = (s0 + b) * kLayerCols + c0;
+    if (c < a.N) {
+      L.lv[b] = ld_stream(a.partial + grow * a.ldc + c);
+#pragma unroll
+      for (int q = 0; q < NP - 1; ++q) L.pv[q][b] = ld_stream(a.peers[q] + grow * a.ldp + c);
+      L.rv[b] = ld_stream(a.residual + orow * a.ldr + c);
+    }
+  }
+}
+
+// Consumes a batch: h = bf16(local + peers in rank order + residual) in fp32,
+// stored to `out` and kept in h[]; returns this thread's sum of squares of
+// the stored h.
+template <int NP>
+__device__ __forceinline__ float layer_consume(const ReduceArgs& a, int64_t orow, int s0, const LayerLoads<NP>& L,
+                                               r_u32x4_t* h) {
+  const int c0 = threadIdx.x * 8;
   float ss = 0.0f;
 #pragma unroll
-  for (int s0 = 0; s0 < kLayerMaxSteps; s0 += B) {
-    if (s0 >= steps) break;
-    r_u32x4_t lv[B], rv[B];
-    r_u32x4_t pv[NP > 1 ? NP - 1 : 1][B];
+  for (int b = 0; b < kLayerBatch; ++b) {
+    const int c = (s0 + b) * kLayerCols + c0;
+    h[s0 + b] = r_u32x4_t{0u, 0u, 0u, 0u};
+    if (c >= a.N) continue;
+    float acc[8];
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int c = (s0 + b) * kLayerCols + c0;
-      if (c < a.N) {
-        lv[b] = ld_stream(a.partial + grow * a.ldc + c);
-#pragma unroll
-        for (int q = 0; q < NP - 1; ++q) pv[q][b] = ld_stream(a.peers[q] + grow * a.ldp + c);
-        rv[b] = ld_stream(a.residual + orow * a.ldr + c);
-      }
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] = __builtin_bit_cast(float, L.lv[b][e] << 16);
+      acc[2 * e + 1] = __builtin_bit_cast(float, L.lv[b][e] & 0xffff0000u);
     }
-    if (s0 == 0) after_first_loads();
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int c = (s0 + b) * kLayerCols + c0;
-      h[s0 + b] = r_u32x4_t{0u, 0u, 0u, 0u};
-      if (c >= a.N) continue;
-      float acc[8];
+    for (int q = 0; q < NP - 1; ++q)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        acc[2 * e] = __builtin_bit_cast(float, lv[b][e] << 16);
-        acc[2 * e + 1] = __builtin_bit_cast(float, lv[b][e] & 0xffff0000u);
+        acc[2 * e] += __builtin_bit_cast(float, L.pv[q][b][e] << 16);
+        acc[2 * e + 1] += __builtin_bit_cast(float, L.pv[q][b][e] & 0xffff0000u);
       }
 #pragma unroll
-      for (int q = 0; q < NP - 1; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] += __builtin_bit_cast(float, pv[q][b][e] << 16);
-          acc[2 * e + 1] += __builtin_bit_cast(float, pv[q][b][e] & 0xffff0000u);
-        }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += __builtin_bit_cast(float, rv[b][e] << 16);
-        acc[2 * e + 1] += __builtin_bit_cast(float, rv[b][e] & 0xffff0000u);
-      }
-      r_u32x4_t o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
-        const float lo = __builtin_bit_cast(float, o[e] << 16);
-        const float hi = __builtin_bit_cast(float, o[e] & 0xffff0000u);
-        ss += lo * lo + hi * hi;
-      }
-      h[s0 + b] = o;
-      __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + orow * a.ldo + c));
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += __builtin_bit_cast(float, L.rv[b][e] << 16);
+      acc[2 * e + 1] += __builtin_bit_cast(float, L.rv[b][e] & 0xffff0000u);
     }
-  }
-  // gamma for every step, issued before the row sum's barrier
-  r_u32x4_t g[kLayerMaxSteps];
-#pragma unroll
-  for (int st = 0; st < kLayerMaxSteps; ++st) {
-    const int c = st * kLayerCols + c0;
-    if (st < steps && c < a.N) g[st] = *reinterpret_cast<const r_u32x4_t*>(a.gamma + c);
-  }
-  ss += __shfl_xor(ss, 32);
-  ss += __shfl_xor(ss, 16);
-  ss += __shfl_xor(ss, 8);
-  ss += __shfl_xor(ss, 4);
-  ss += __shfl_xor(ss, 2);
-  ss += __shfl_xor(ss, 1);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  static_assert(kLayerThreads == 256, "four wave sums");
-  const float rstd = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) * (1.0f / static_cast<float>(a.N)) + a.eps);
-#pragma unroll
-  for (int st = 0; st < kLayerMaxSteps; ++st) {
-    const int c = st * kLayerCols + c0;
-    if (st >= steps || c >= a.N) continue;
     r_u32x4_t o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float lo = __builtin_bit_cast(float, h[st][e] << 16) * rstd * __builtin_bit_cast(float, g[st][e] << 16);
-      const float hi = __builtin_bit_cast(float, h[st][e] & 0xffff0000u) * rstd *
-                       __builtin_bit_cast(float, g[st][e] & 0xffff0000u);
-      o[e] = rnd_pack_bf16x2(lo, hi);
+      o[e] = rnd_pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+      const float lo = __builtin_bit_cast(float, o[e] << 16);
+      const float hi = __builtin_bit_cast(float, o[e] & 0xffff0000u);
+      ss += lo * lo + hi * hi;
     }
-    __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.y + orow * a.ldy + c));
+    h[s0 + b] = o;
+    __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.out + orow * a.ldo + c));
   }
+  return ss;
 }
 
 // The layer epilogue's task loop (blockDim.x == kLayerThreads): output rows
 // taken from the device counter in order, each once all tiles of its tile
 // row are published; counters returned to zero as in reducer_dynamic.
-// s: eight ints of LDS.
+// Rows are pipelined: once a row's h is stored, wave 0 takes the next row
+// and checks its tile row's flags; if they are all in, the next row's loads
+// are issued right after the workgroup barrier that folds the current row's
+// sum of squares, before the current row's y is computed and stored, so the
+// workgroup keeps loads in flight between rows.  Otherwise the next row
+// waits at the top of the loop as the first one does.
+// s: sixteen ints of LDS (task ids, early-issue flags, two sets of row sums).
 template <int NP>
 __device__ __forceinline__ void reducer_layer(const ReduceArgs& a, int* s, unsigned int taken) {
   const int tiles_n = a.N / kTile;
   const int ntiles = (a.M / kTile) * tiles_n;
+  const int steps = (a.N + kLayerCols - 1) / kLayerCols;
   const int64_t first_row = a.dest >= 0 ? static_cast<int64_t>(a.dest) * (a.M / NP) : 0;
   auto tile_row = [&](int task) { return static_cast<int>((first_row + task) / kTile); };
-  float* red = reinterpret_cast<float*>(s + 4);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float* red = reinterpret_cast<float*>(s + 8);   // [2][4]: row sums, alternating by row
+  // gamma is the same for every row: loaded once, kept in registers (an
+  // input of the call, so no acquire orders it).
+  r_u32x4_t g[kLayerMaxSteps];
+#pragma unroll
+  for (int st = 0; st < kLayerMaxSteps; ++st) {
+    const int c = st * kLayerCols + threadIdx.x * 8;
+    g[st] = c < a.N ? *reinterpret_cast<const r_u32x4_t*>(a.gamma + c) : r_u32x4_t{0u, 0u, 0u, 0u};
+  }
   __syncthreads();   // producer waves are done with the LDS
   if (threadIdx.x == 0) s[0] = static_cast<int>(taken != ~0u ? taken : atomicAdd(a.task_ctr, 1u));
   __syncthreads();
   int task = s[0];
-  bool timed_out = false;              // wave 0
-  bool have_poll = false, polled = false;   // wave 0: a poll of this task's tile row made early
+  bool timed_out = false;   // wave 0
+  bool issued = false;      // this task's first batch of loads is in flight
+  int parity = 0;
+  LayerLoads<NP> L;
   while (task < a.ntasks) {
-    const int tr = tile_row(task);
-    if (threadIdx.x < 64) {
-      if (threadIdx.x == 0) s[1] = static_cast<int>(atomicAdd(a.task_ctr, 1u));   // next task, early
-      if (!timed_out) {
-        const bool ok = have_poll ? polled : row_flags_ready<NP>(a, tr, tiles_n, ntiles);
-        timed_out = !wave_await_row<NP>(a, tr, tiles_n, ntiles, ok);
+    if (!issued) {
+      if (threadIdx.x < 64) {
+        const int tr = tile_row(task);
+        if (!timed_out) timed_out = !wave_await_row<NP>(a, tr, tiles_n, ntiles, row_flags_ready<NP>(a, tr, tiles_n, ntiles));
+        if (lane == 0) acquire_fence();
       }
-      if ((threadIdx.x & 63) == 0) acquire_fence();
+      __syncthreads();
+      layer_issue<NP>(a, task, 0, L);
     }
-    __syncthreads();
-    const int next = s[1];
-    have_poll = false;
-    layer_row<NP>(a, task, red, [&] {
-      if (threadIdx.x < 64 && next < a.ntasks && !timed_out) {
-        polled = row_flags_ready<NP>(a, tile_row(next), tiles_n, ntiles);
-        have_poll = true;
+    // The next task, taken while this row's loads are in flight.
+    int next_w0 = 0;
+    if (threadIdx.x < 64) {
+      const unsigned int nx = lane == 0 ? atomicAdd(a.task_ctr, 1u) : 0u;
+      next_w0 = static_cast<int>(__shfl(nx, 0));
+    }
+    r_u32x4_t h[kLayerMaxSteps];
+    float ss = layer_consume<NP>(a, task, 0, L, h);
+#pragma unroll
+    for (int s0 = kLayerBatch; s0 < kLayerMaxSteps; s0 += kLayerBatch) {
+      if (s0 < steps) {
+        layer_issue<NP>(a, task, s0, L);
+        ss += layer_consume<NP>(a, task, s0, L, h);
+      } else {
+#pragma unroll
+        for (int b = 0; b < kLayerBatch; ++b) h[s0 + b] = r_u32x4_t{0u, 0u, 0u, 0u};
       }
-    });
-    __syncthreads();   // s[1] and the row sums are rewritten next
+    }
+    // Wave 0: are the next row's flags all in?  Then acquire now.
+    if (threadIdx.x < 64) {
+      bool ready = false;
+      if (next_w0 < a.ntasks && !timed_out) {
+        ready = __ballot(!row_flags_ready<NP>(a, tile_row(next_w0), tiles_n, ntiles)) == 0;
+        if (ready && lane == 0) acquire_fence();
+      }
+      if (lane == 0) {
+        s[1 + parity] = next_w0;
+        s[3 + parity] = ready;
+      }
+    }
+    ss += __shfl_xor(ss, 32);
+    ss += __shfl_xor(ss, 16);
+    ss += __shfl_xor(ss, 8);
+    ss += __shfl_xor(ss, 4);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 1);
+    if (lane == 0) red[4 * parity + wave] = ss;
+    __syncthreads();   // row sums, the next task and its readiness are visible; loads after the acquire
+    static_assert(kLayerThreads == 256, "four wave sums");
+    const float* rs = red + 4 * parity;
+    const float rstd = rsqrtf(((rs[0] + rs[1]) + (rs[2] + rs[3])) * (1.0f / static_cast<float>(a.N)) + a.eps);
+    const int next = s[1 + parity];
+    const bool early = s[3 + parity] != 0;
+    if (early) layer_issue<NP>(a, next, 0, L);
+#pragma unroll
+    for (int st = 0; st < kLayerMaxSteps; ++st) {
+      const int c = st * kLayerCols + threadIdx.x * 8;
+      if (st >= steps || c >= a.N) continue;
+      r_u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __builtin_bit_cast(float, h[st][e] << 16) * rstd * __builtin_bit_cast(float, g[st][e] << 16);
+        const float hi = __builtin_bit_cast(float, h[st][e] & 0xffff0000u) * rstd *
+                         __builtin_bit_cast(float, g[st][e] & 0xffff0000u);
+        o[e] = rnd_pack_bf16x2(lo, hi);
+      }
+      __builtin_nontemporal_store(o, reinterpret_cast<r_u32x4_t*>(a.y + task * a.ldy + c));
+    }
     task = next;
+    issued = early;
+    parity ^= 1;
   }
   if (threadIdx.x == 0 && atomicAdd(a.task_ctr + 1, 1u) == gridDim.x - 1) {
     atomicExch(a.task_ctr, 0u);
