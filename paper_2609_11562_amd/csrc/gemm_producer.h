@@ -486,7 +486,12 @@ __device__ __forceinline__ unsigned int producer_body(const GemmArgs& a, const i
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
     for (int kt = 0; kt < nk; ++kt) step(g++);
 
-    if (a.take_ctr && tid == 0 && lb + 1 == mine) taken = atomicAdd(a.take_ctr, 1u);
+    // Taken by thread 0 and made wave-uniform, so it waits in a scalar
+    // register (meaningful in wave 0 only).
+    if (a.take_ctr && wave == 0 && lb + 1 == mine) {
+      const unsigned int t = tid == 0 ? atomicAdd(a.take_ctr, 1u) : 0u;
+      taken = __builtin_amdgcn_readfirstlane(t);
+    }
 
     // ---- epilogue.  Lane holds D[n][m] for m = lane % 32 and
     // n = 8 (v / 4) + 4 (lane / 32) + v % 4, v = 0..15 (D = C^T): 4

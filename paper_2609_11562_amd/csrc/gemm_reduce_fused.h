@@ -34,9 +34,11 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   __shared__ __attribute__((aligned(1024))) char smem[GemmShape<BM, BN>::LDS_BYTES];
   const int b = blockIdx.x;
   // Stamps are stored as they are taken, so none stays live in registers
-  // across the producer.
-  unsigned long long* const st = stamps && threadIdx.x == 0 ? stamps + kStampsPerWg * b : nullptr;
-  if (st) {
+  // across the producer; their address is recomputed from the (scalar)
+  // kernel arguments at each use.
+  const bool stamp = stamps != nullptr && threadIdx.x == 0;
+  if (stamp) {
+    unsigned long long* const st = stamps + kStampsPerWg * b;
     st[0] = wall_clock64();
     st[4] = __builtin_amdgcn_s_memtime();
     if (b >= G) {
@@ -46,7 +48,8 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   }
   publish_peer_slice(r, np, b, gridDim.x);
   const unsigned int taken = b < G ? producer_body<BM, BN, TAIL>(g, b, G, smem) : ~0u;
-  if (st && b < G) {
+  if (stamp && b < G) {
+    unsigned long long* const st = stamps + kStampsPerWg * b;
     st[1] = wall_clock64();
     st[5] = __builtin_amdgcn_s_memtime();
   }
@@ -78,7 +81,8 @@ __global__ __launch_bounds__(256) void gemm_reduce_fused(GemmArgs g, ReduceArgs 
   }
   if (stamps) {
     __syncthreads();
-    if (st) {
+    if (stamp) {
+      unsigned long long* const st = stamps + kStampsPerWg * b;
       if (r.layer) st[2] = 0;
       st[3] = wall_clock64();
     }
