@@ -54,10 +54,11 @@ def check_layer(prob, R_bits, gamma, h_bits, y_bits, grow, lrow):
         assert not bad.any(), f"{name}: bound exceeded at {np.argwhere(bad)[:5].tolist()}"
 
 
-@pytest.mark.parametrize("dest,N", [(1, 1024), (E.DEST_ALL, 1024), (2, 3200)])
+@pytest.mark.parametrize("dest,N", [(1, 1024), (E.DEST_ALL, 1024), (2, 3200), (0, 16384), (3, 12416)])
 def test_layer_matches_oracle_and_reducer_arithmetic(dest, N):
     """N = 3200 leaves a ragged last step of columns (a row is walked 2048
-    columns at a time)."""
+    columns at a time); N above 8192 takes a second batch of loads per row
+    (16384 the largest row, 12416 with a ragged last step)."""
     M, K, P = 1024, 256, 4
     print(f"[layer small dest={dest} N={N}]", flush=True)
     prob = make_problem(M, N, K, P, Dist("normal", 0.02), Dist("normal", 0.02), seed=31)
