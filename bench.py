@@ -281,6 +281,19 @@ def main():
         _, p_f = timed("fused", n_leg, w_leg)
         _, p_rm = timed("gemm_row_major", n_leg, w_leg)
         med = statistics.median
+        # For comparison only: the vendor library's plain GEMM (torch.matmul,
+        # hipBLASLt) on the same operands, timed with events on this stream.
+        lib_c = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+        for _ in range(w_leg):
+            torch.matmul(A, B, out=lib_c)
+        ev_a, ev_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev_a.record(gs)
+        for _ in range(n_leg):
+            torch.matmul(A, B, out=lib_c)
+        ev_b.record(gs)
+        torch.cuda.synchronize()
+        T_lib = ev_a.elapsed_time(ev_b) / n_leg
+        del lib_c
         T_G = med([p[0] for p in p_g])
         T_R = med([p[1] for p in p_r])
         T_seq = med([p[2] for p in p_s])
@@ -298,6 +311,8 @@ def main():
             "B_req_GBps": ((P - 1) / P) * M * N * 2 / (med([p[0] for p in p_f]) * 1e-3) / 1e9,
             "gemm_alone_tflops": flops / (T_G * 1e-3) / 1e12,
             "T_gemm_row_major_ms": med([p[0] for p in p_rm]),
+            "T_library_gemm_ms": T_lib,          # torch.matmul (hipBLASLt), comparison only
+            "library_gemm_tflops": flops / (T_lib * 1e-3) / 1e12,
             # the paper's measured communication bandwidth: the reduction's
             # bytes over the elapsed time of the call that contains it
             "reducer_in_fused_GBps": rbytes / (T_fused * 1e-3) / 1e9,
