@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--release-blocks", type=int, default=None,
                     help="producer blocks per release (-1 = once per workgroup)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--timeline", action="store_true",
+                    help="add the single launch's per-workgroup timeline (medians over the last timed calls)")
     ap.add_argument("--no-legs", action="store_true", help="skip the gemm-only / reduce-only / sequential legs")
     ap.add_argument("--only", default=None, choices=["fused", "gemm", "reduce", "seq", "plain"],
                     help="time just one mode (for profiler runs)")
@@ -203,6 +205,9 @@ def main():
     clock_ghz = None
     if main_mode in ("fused", "plain") and cfg.launch == 0:
         clock_ghz = statistics.median(ctx.last_clock(b) for b in range(min(args.steps, 255)))
+    timeline = None
+    if args.timeline and main_mode in ("fused", "plain") and cfg.launch == 0:
+        timeline = workgroup_timeline(ctx, min(args.steps, 20))
     g_ms = [p[0] for p in per if p[0] > 0]
     r_ms = [p[1] for p in per if p[1] > 0]
     e_ms = [p[2] for p in per if p[2] > 0]
@@ -385,12 +390,48 @@ def main():
         "cpu_baseline": cpu,
         "overlap": legs,
         "ranks": ranks,
+        "timeline": timeline,
         "input_gen_s": round(t_gen, 2),
         "device": device_info(torch, M, N, cfg),
     }
     if copy:
         rec["copy_calibration"] = copy
     print(json.dumps(rec), flush=True)
+
+
+def workgroup_timeline(ctx, ncalls):
+    """Medians over the last `ncalls` single-launch calls of where the time
+    goes per workgroup, in microseconds from the first workgroup's start:
+    when producers finish (first, median, last), when dedicated reducers and
+    producers start their first reduction task, and when the last workgroup
+    ends.  Shows whether the reduction runs during the GEMM window or after
+    it."""
+    import numpy as np
+    rows = []
+    for back in range(ncalls):
+        us, G = ctx.last_stamps(back)
+        prod_end = us[:G, 1]
+        ready = us[:, 2]
+        ded = ready[G:]
+        ded = ded[~np.isnan(ded)]
+        prod_ready = ready[:G]
+        prod_ready = prod_ready[~np.isnan(prod_ready)]
+        rows.append({
+            "workgroups": int(us.shape[0]), "producers": int(G),
+            "producer_end_first": float(prod_end.min()) if G else None,
+            "producer_end_median": float(np.median(prod_end)) if G else None,
+            "producer_end_last": float(prod_end.max()) if G else None,
+            "dedicated_first_task_ready_median": float(np.median(ded)) if ded.size else None,
+            "producer_first_task_ready_median": float(np.median(prod_ready)) if prod_ready.size else None,
+            "end_last": float(us[:, 3].max()),
+        })
+    out = {}
+    for k in rows[0]:
+        vals = [r[k] for r in rows if r[k] is not None]
+        out[k] = (round(statistics.median(vals), 2) if isinstance(vals[0], float) else vals[0]) if vals else None
+    out["calls"] = len(rows)
+    out["unit"] = "us from the first workgroup's start"
+    return out
 
 
 def device_info(torch, M, N, cfg):
