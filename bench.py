@@ -131,6 +131,9 @@ def main():
         if v is not None:
             kw[k] = v
     cfg = E.Config.make(**kw, record_timing=1)
+    # The timed loop runs without per-call events or workgroup stamps; a
+    # second, untimed pass with them supplies the per-call diagnostics.
+    cfg_timed = E.Config.make(**kw, record_timing=0)
     # The non-overlapped legs give the reduction the whole device (two-stream
     # kernels, budget capped by the library at min(tiles per chunk, CUs - 1)).
     cfg_seq = E.Config.make(**dict(kw, launch=1, reduce_wgs=255, reduce_threads=1024), record_timing=1)
@@ -161,13 +164,14 @@ def main():
                "h_unfused": {d: torch.empty_like(o) for d, o in outs.items()},
                "y_unfused": {}}
 
-    def step(i, mode="fused"):
+    def step(i, mode="fused", c=None):
         d = dest_of(i)
+        c = c or cfg
         if mode == "fused" and layer:
             ctx.gemm_rs_rmsnorm(A, B, peers, d, lay["R"], lay["gamma"], lay["eps"], h_out=lay["h"][d],
-                                y_out=lay["y"][d], partial=partial, cfg=cfg, stream=gs)
+                                y_out=lay["y"][d], partial=partial, cfg=c, stream=gs)
         elif mode in ("fused", "plain"):
-            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg, gemm_stream=gs, reduce_stream=rs)
+            ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=c, gemm_stream=gs, reduce_stream=rs)
         elif mode == "seq":
             ctx.gemm_rs(A, B, peers, d, out=outs[d], partial=partial, cfg=cfg_seq, gemm_stream=gs, reduce_stream=gs)
         elif mode == "layer_unfused":
@@ -176,7 +180,7 @@ def main():
             h = torch.add(outs[d], lay["R"], out=lay["h_unfused"][d])
             lay["y_unfused"][d] = torch.nn.functional.rms_norm(h, (N,), lay["gamma"], lay["eps"])
         elif mode == "gemm":
-            ctx.gemm_only(A, B, partial=partial, cfg=cfg, stream=gs)
+            ctx.gemm_only(A, B, partial=partial, cfg=c, stream=gs)
         elif mode == "gemm_row_major":
             ctx.gemm_only(A, B, partial=partial, cfg=cfg_rm, stream=gs)
         else:
@@ -198,16 +202,40 @@ def main():
         per = [ctx.last_timing(b) for b in range(n)]
         return wall, per
 
+    def timed_plain(mode, steps, warmup):
+        """Host wall clock per step, and HIP events on the launch stream
+        around the whole loop, with no per-call instrumentation."""
+        c = cfg_timed if mode in ("fused", "plain", "gemm") else None
+        for i in range(warmup):
+            step(i, mode, c)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record(gs)
+        for i in range(steps):
+            step(i, mode, c)
+        ev1.record(gs)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        st = ctx.query_status()
+        if st[0] != E.OK:
+            raise SystemExit(f"bench.py: reducer reported status {st}")
+        return wall, ev0.elapsed_time(ev1) / steps
+
     main_mode = args.only or "fused"
-    ms_per_step, per = timed(main_mode, args.steps, args.warmup)
+    ms_per_step, loop_ms = timed_plain(main_mode, args.steps, args.warmup)
+    # Diagnostics: the same calls again with per-call events and the
+    # workgroups' stamps (not part of the timed loop).
+    n_diag = min(args.steps, 100)
+    _, per = timed(main_mode, n_diag, 5)
     # Engine clock of the producer role over the timed single-launch calls
     # (engine cycles over wall-clock time, from the workgroups' own stamps).
     clock_ghz = None
     if main_mode in ("fused", "plain") and cfg.launch == 0:
-        clock_ghz = statistics.median(ctx.last_clock(b) for b in range(min(args.steps, 255)))
+        clock_ghz = statistics.median(ctx.last_clock(b) for b in range(n_diag))
     timeline = None
     if args.timeline and main_mode in ("fused", "plain") and cfg.launch == 0:
-        timeline = workgroup_timeline(ctx, min(args.steps, 20))
+        timeline = workgroup_timeline(ctx, min(n_diag, 20))
     g_ms = [p[0] for p in per if p[0] > 0]
     r_ms = [p[1] for p in per if p[1] > 0]
     e_ms = [p[2] for p in per if p[2] > 0]
@@ -222,7 +250,7 @@ def main():
         by_rank = {}
         for back, p in enumerate(per):
             if p[2] > 0:
-                by_rank.setdefault(dest_of(args.steps - 1 - back), []).append(p[2])
+                by_rank.setdefault(dest_of(n_diag - 1 - back), []).append(p[2])
         med_r = {d: statistics.median(v) for d, v in sorted(by_rank.items())}
         worst = max(med_r.values())
         ranks = {"per_rank_ms": [round(med_r[d], 5) for d in sorted(med_r)], "max_ms": round(worst, 5),
@@ -230,10 +258,13 @@ def main():
                  "tflops_at_max": round(flops / (worst * 1e-3) / 1e12, 2)}
     mean_g = statistics.fmean(g_ms) if g_ms else None
     # Dominant kernel: the single fused launch (both roles) when the path runs
-    # as one kernel, else the producer.  Its mean duration comes from HIP
-    # events recorded on the stream it is launched on, inside the timed loop.
+    # as one kernel, else the producer.  Its mean duration: HIP events on the
+    # stream it is launched on around the timed loop, over the launches (the
+    # single launch and the producer alone), else the per-call events of the
+    # diagnostic pass.
     single = main_mode in ("fused", "plain") and cfg.launch == 0
-    mean_k = statistics.fmean(e_ms) if single and e_ms else mean_g
+    mean_k = loop_ms if single or main_mode == "gemm" else mean_g
+    per_call_k = statistics.fmean(e_ms) if single and e_ms else None
     kernel = "gemm_reduce_fused" if single else "gemm_producer"
     achieved = flops / (mean_k * 1e-3) / 1e12 if mean_k else None
     root = os.path.dirname(os.path.abspath(__file__))
@@ -385,6 +416,7 @@ def main():
                      "traffic_detail": traffic,
                      "algorithmic_bytes": round(algo_bytes),
                      "kernel_mean_ms": round(mean_k, 5) if mean_k else None,
+                     "kernel_mean_ms_per_call_events": round(per_call_k, 5) if per_call_k else None,
                      "producer_span_ms": round(mean_g, 5) if mean_g else None,
                      "producer_tflops": round(flops / (mean_g * 1e-3) / 1e12, 2) if mean_g else None},
         "cpu_baseline": cpu,
