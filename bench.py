@@ -130,6 +130,8 @@ def main():
                  ("launch", args.launch), ("release_blocks", args.release_blocks)):
         if v is not None:
             kw[k] = v
+    if kw.get("launch", 0) != 0 and kw.get("reduce_wgs") == -1 and args.x is None:
+        kw["reduce_wgs"] = 0   # "no dedicated reducers" exists only in the single launch
     cfg = E.Config.make(**kw, record_timing=1)
     # The timed loop runs without per-call events or workgroup stamps; a
     # second, untimed pass with them supplies the per-call diagnostics.
